@@ -1,0 +1,37 @@
+"""Algorithmic work and traffic of one chunkwise delta-rule prefill.
+
+Counts per (token, value head) with chunk size C and head dims d_k, d_v; these
+are the units the roofline fractions are quoted in.
+
+MACs, chunkwise form (paper Sec. 2.1 operators #2-#6 and Sec. 5's GEMM set
+KS, QS, KK^T, QK^T): KK^T, QK^T, T.(K*e^gamma), T.V and P.U each cost C*d per
+token; W.H, K~^T.U and Q.H each cost d_k*d_v; the triangular solve costs about
+C^2/2.  With C = 64 and d = 128 this is 92,160 MAC per token-head, which
+reproduces the paper's Table 1 linear-attention MAC column exactly.
+
+Bytes (algorithmic): what the method itself must move once -- read q, k, v,
+gate, beta (and s0 when given), write o and the final state.
+"""
+
+from __future__ import annotations
+
+
+def macs_per_token_head(C: int = 64, dk: int = 128, dv: int = 128) -> float:
+    # the C*d terms: KK^T and QK^T contract over d_k; the T.K, T.V and P.U
+    # terms produce d_k or d_v columns.
+    cd = 2 * C * dk + C * dk + C * dv + C * dv
+    dd = 3 * dk * dv
+    return float(cd + dd + C * C / 2)
+
+
+def flops(T_total: int, Hv: int, C: int = 64, dk: int = 128, dv: int = 128) -> float:
+    return 2.0 * macs_per_token_head(C, dk, dv) * T_total * Hv
+
+
+def algorithmic_bytes(T_total: int, N: int, Hqk: int, Hv: int, dk: int, dv: int,
+                      elt_bytes: int, kda: bool, with_s0: bool) -> int:
+    """q, k, v, o in the I/O dtype; g, beta fp32; s0 (if given) and s_final fp32."""
+    per_token = (2 * Hqk * dk + 2 * Hv * dv) * elt_bytes          # q, k, v, o
+    per_token += Hv * 4 * (dk if kda else 1) + Hv * 4              # gate, beta
+    state = N * Hv * dk * dv * 4
+    return per_token * T_total + state * (2 if with_s0 else 1)
