@@ -1,0 +1,185 @@
+#!/usr/bin/env python3
+"""Throughput of GDN prefill on one MI355X: tokens/s, roofline fraction, CPU oracle beside it.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload 1] [--no-cpu-baseline]
+
+One step = one full gdn_prefill call (chunk index, chunk-local, state
+propagation, output) over the workload: by default one sequence of 4096
+tokens, 16 heads, head dim 128, bf16 q/k/v, fp32 gates and state (seeded
+synthetic inputs, see paper_2609_32114_amd/inputs.py).  Inputs are resident in
+HBM before timing; the step cycles through several input copies (more bytes
+than the 256 MB Infinity Cache) so each step reads its inputs from HBM, not
+from cache.  Per-kernel times come from HIP events recorded by the library on
+the launch stream inside the timed region.
+
+Prints ONE JSON line.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "GDN prefill tokens/s at H=16,d=128,T=4096 bf16; % of HBM/MFMA roofline"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def kernel_source_hash(name: str) -> str:
+    """Hash of the sources a kernel is built from (traffic counters go stale when they change)."""
+    csrc = os.path.join(ROOT, "paper_2609_32114_amd", "csrc")
+    files = {"chunk_local": "k1_chunk_local.hip", "state_prop": "k2_state_prop.hip",
+             "output": "k3_output.hip", "chunk_index": "k0_chunk_index.hip"}
+    h = hashlib.sha256()
+    for f in (files[name], "device.h", "prefill.h"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 PMC counts, if still current."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f).get(f"{kernel}@{workload}")
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_hash") != kernel_source_hash(kernel):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(inp, budget_s=10.0, max_reps=40):
+    import oracle
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    oracle.build(force=False)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.run_inputs(inp, nthreads=threads)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or reps >= max_reps:
+            break
+    tokens = reps * inp.T
+    return {"value": tokens / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"full workload ({inp.T} tokens x {inp.v.shape[1]} heads) repeated "
+                      f"{reps}x, {el:.1f} s, fp64 token recurrence"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=1)
+    ap.add_argument("--copies", type=int, default=6)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the method shards by (sequence, head) with no "
+              "communication, so a multi-GPU figure would be N independent copies of this run; "
+              "run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_32114_amd as P
+    from paper_2609_32114_amd import cost
+    from paper_2609_32114_amd.inputs import WORKLOADS, make_workload
+
+    P.load_library()
+    wl = WORKLOADS[args.workload]
+    inp = make_workload(args.workload)
+    kda = inp.kind == "kda"
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    dt = torch.bfloat16 if inp.dtype == "bf16" else torch.float32
+    esz = 2 if inp.dtype == "bf16" else 4
+    T, N = inp.T, inp.N
+    Hqk, Hv, Dk, Dv = wl.Hqk, wl.Hv, wl.Dk, wl.Dv
+
+    def dev_copy(seed_shift):
+        t = lambda x, d=torch.float32: torch.from_numpy(np.ascontiguousarray(x)).to(dev).to(d)
+        return dict(q=t(inp.q, dt), k=t(inp.k, dt), v=t(inp.v, dt), g=t(inp.g), beta=t(inp.beta),
+                    s0=None if inp.s0 is None else t(inp.s0))
+
+    copies = [dev_copy(i) for i in range(max(1, args.copies))]
+    cu = torch.from_numpy(inp.cu_seqlens).to(dev)
+    fn = P.gdn_prefill if not kda else P.kda_prefill
+    ws = torch.empty(P.workspace_size(inp.kind, N, T, Hqk, Hv, Dk, Dv,
+                                      P.HAGDN_BF16 if esz == 2 else P.HAGDN_F32),
+                     dtype=torch.uint8, device=dev)
+    o = torch.empty((T, Hv, Dv), dtype=dt, device=dev)
+    sf = torch.empty((N, Hv, Dk, Dv), dtype=torch.float32, device=dev)
+
+    def step(i):
+        c = copies[i % len(copies)]
+        fn(c["q"], c["k"], c["v"], c["g"], c["beta"], initial_state=c["s0"], cu_seqlens=cu,
+           scale=inp.scale, workspace=ws, out=o, final_out=sf)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    P.profile_begin(args.steps)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        step(args.warmup + i)
+    end.record()
+    torch.cuda.synchronize()
+    kernel_ms, ncalls = P.profile_end()
+    ms = start.elapsed_time(end) / args.steps
+
+    value = T / (ms * 1e-3)
+    dom = max(kernel_ms, key=kernel_ms.get)
+    dom_bytes = cost.kernel_bytes(dom, T, N, Hqk, Hv, Dk, Dv, esz, kda, inp.s0 is not None)
+    dom_ms = kernel_ms[dom]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    traffic = measured_traffic(dom, wl.name)
+    path_bytes = cost.algorithmic_bytes(T, N, Hqk, Hv, Dk, Dv, esz, kda, inp.s0 is not None)
+    path_flops = cost.flops(T, Hv, 64, Dk, Dv)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": inp.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "kind": inp.kind, "sequences": N, "seq_len": T,
+                   "q_k_heads": Hqk, "v_heads": Hv, "head_dim_k": Dk, "head_dim_v": Dv,
+                   "chunk": 64, "input_copies": len(copies)},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "bytes_per_launch": dom_bytes, "kernel_ms": dom_ms},
+        "path_roofline": {"bound": "hbm", "algorithmic_bytes": path_bytes,
+                          "achieved": path_bytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
+                          "unit": "GB/s", "frac": path_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                          "flops": path_flops,
+                          "mfma_frac": path_flops / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
+        "kernels_ms": kernel_ms,
+        "kernel_calls_timed": ncalls,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(inp)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,137 @@
+/*
+ * hagdn.h -- C ABI of the MI355X (gfx950) chunkwise delta-rule prefill library.
+ *
+ * The operation (paper, Sec. 2.1 "Architecture of Linear-Attention Hybrids"
+ * and "Chunkwise Map-Reduce-Map Execution"): prefill of a delta-rule
+ * linear-attention layer.  Per sequence n and value head h a d_k x d_v state
+ * is carried token by token; with S the state in d_v x d_k orientation,
+ *
+ *   Gated DeltaNet (GDN):  S_t = a_t S_{t-1} (I - b_t k_t k_t^T) + b_t v_t k_t^T
+ *   KDA:                   S_t = S_{t-1} Diag(a_t) (I - b_t k_t k_t^T) + b_t v_t k_t^T
+ *   output (both):         o_t = scale * S_t q_t       (reads the UPDATED state)
+ *
+ * where a_t = exp(g_t) is a scalar per (token, head) for GDN and a vector of
+ * d_k per-key-channel decays for KDA.  The library computes this with the
+ * chunkwise Map-Reduce-Map decomposition (chunk length 64, the paper's
+ * setting in Sec. 7.1): operators #1-#4 (Gate, KKT, Solve, W/U) chunk-parallel,
+ * operator #5 (H) sequential over chunks, operator #6 (O) chunk-parallel.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers.  Every tensor pointer is a DEVICE pointer (HIP device memory of
+ *   the current device), row-major, contiguous.  The caller owns every buffer,
+ *   including the workspace.  The library never allocates or frees device
+ *   memory, never synchronises the stream (except hagdn_device_status), and
+ *   keeps no pointer after returning.  When T = 0 the token tensors (q, k, v,
+ *   g, beta, o) are never read or written and may be NULL.
+ * Layouts (T = T_total packed tokens, sequences delimited by cu_seqlens):
+ *   q, k        [T, Hqk, Dk]   dtype
+ *   v, o        [T, Hv,  Dv]   dtype
+ *   g (GDN)     [T, Hv]        fp32 log-gate, a_t = exp(g) (g <= 0 expected)
+ *   g (KDA)     [T, Hv, Dk]    fp32 per-key-channel log-gate
+ *   beta        [T, Hv]        fp32 write strength
+ *   s0, s_final [N, Hv, Dk, Dv] fp32, the state stored as S^T (row = key
+ *               channel, d_v contiguous).  s0 == NULL means a zero initial
+ *               state; s_final == NULL skips writing the final state.
+ *               s_final may alias s0 exactly (in-place update); no other
+ *               aliasing between arguments is allowed.
+ *   cu_seqlens  [N+1] int32, DEVICE memory: cu[0] = 0, cu[N] = T,
+ *               nondecreasing.  Zero-length sequences are allowed.  Chunks
+ *               restart at every sequence start; no chunk spans two sequences.
+ * Grouped heads: value head h reads q/k head h / (Hv / Hqk).
+ * Supported shapes: Dk, Dv in {64, 128}; Hv % Hqk == 0; N >= 1; T >= 0.
+ * dtype: HAGDN_BF16 (q/k/v/o bf16; fp32 state and accumulation, bf16
+ *   intermediates) or HAGDN_F32 (everything fp32).
+ * Alignment: q, k, v, o, s0, s_final and workspace 16-byte aligned; g, beta
+ *   and cu_seqlens 4-byte aligned.
+ * stream: a hipStream_t passed as void* (NULL = the default stream).  Work is
+ *   enqueued asynchronously in stream order.
+ * Errors: every entry point returns a hagdn_status.  Arguments are checked on
+ *   the host before anything is enqueued; on a non-OK return nothing was
+ *   launched (except HAGDN_EHIP: a launch failed) and hagdn_last_error()
+ *   describes the problem.  Contents of cu_seqlens live on the device and are
+ *   checked by the first kernel: if they are malformed, no token is processed
+ *   (o is left untouched, s_final receives s0 or zeros) and
+ *   hagdn_device_status() reports HAGDN_DEV_BAD_SEQLENS afterwards.
+ */
+#ifndef HAGDN_H
+#define HAGDN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HAGDN_OK = 0,
+  HAGDN_EINVAL = 1,        /* NULL required pointer, bad count, misalignment */
+  HAGDN_EUNSUPPORTED = 2,  /* head dim / dtype outside the supported set     */
+  HAGDN_EWORKSPACE = 3,    /* workspace smaller than *_workspace_size()      */
+  HAGDN_EHIP = 4           /* a HIP runtime call or kernel launch failed     */
+} hagdn_status;
+
+typedef enum { HAGDN_F32 = 0, HAGDN_BF16 = 1 } hagdn_dtype;
+
+/* Device-side status word written by the first kernel of every call. */
+typedef enum { HAGDN_DEV_OK = 0, HAGDN_DEV_BAD_SEQLENS = 1 } hagdn_device_code;
+
+/* Bytes of device workspace gdn_prefill needs for these sizes (0 if the
+ * arguments are invalid; hagdn_last_error() then says why).  The workspace
+ * holds the chunk index and the per-chunk intermediates of operators #1-#5
+ * (W, U~ and the decayed keys of Sec. 5's rewrite, the state snapshots S_c and
+ * the corrected values v_c that operator #6 reads). */
+size_t gdn_prefill_workspace_size(int N, int T_total, int Hqk, int Hv, int Dk,
+                                  int Dv, int dtype);
+
+/* Gated DeltaNet prefill (scalar log-gate per token and value head).
+ * Computes o [T, Hv, Dv] and, if s_final != NULL, the final states. */
+int gdn_prefill(const void *q, const void *k, const void *v, const float *g,
+                const float *beta, const float *s0, const int32_t *cu_seqlens,
+                int N, int T_total, int Hqk, int Hv, int Dk, int Dv,
+                float scale, int dtype, void *o, float *s_final,
+                void *workspace, size_t workspace_bytes, void *stream);
+
+/* Workspace bytes for kda_prefill (same meaning as above). */
+size_t kda_prefill_workspace_size(int N, int T_total, int Hqk, int Hv, int Dk,
+                                  int Dv, int dtype);
+
+/* KDA prefill: as gdn_prefill, but g is the per-key-channel log-gate
+ * [T, Hv, Dk]; the decay Diag(exp(g_t)) acts on the key side of the state
+ * before the delta update. */
+int kda_prefill(const void *q, const void *k, const void *v, const float *g,
+                const float *beta, const float *s0, const int32_t *cu_seqlens,
+                int N, int T_total, int Hqk, int Hv, int Dk, int Dv,
+                float scale, int dtype, void *o, float *s_final,
+                void *workspace, size_t workspace_bytes, void *stream);
+
+/* Message for the last non-OK return on this host thread ("" if none). */
+const char *hagdn_last_error(void);
+
+/* Reads the device status word that the most recent call using this
+ * workspace wrote.  Synchronises `stream`.  *code receives a
+ * hagdn_device_code.  Returns HAGDN_OK, HAGDN_EINVAL or HAGDN_EHIP. */
+int hagdn_device_status(const void *workspace, size_t workspace_bytes,
+                        void *stream, int *code);
+
+/* Per-kernel timing with HIP events recorded on the call's stream around each
+ * kernel of every gdn_prefill / kda_prefill call made on this host thread
+ * between begin and end (at most max_calls calls are recorded; later calls run
+ * untimed).  hagdn_profile_end synchronises the recorded events and writes,
+ * for each kernel i < min(max_kernels, hagdn_kernel_count()), the mean
+ * duration in milliseconds into mean_ms[i]; *calls receives the number of
+ * calls timed.  Returns a hagdn_status. */
+int hagdn_profile_begin(int max_calls);
+int hagdn_profile_end(double *mean_ms, int max_kernels, int *calls);
+int hagdn_kernel_count(void);
+const char *hagdn_kernel_name(int i);
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int hagdn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HAGDN_H */

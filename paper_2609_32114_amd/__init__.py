@@ -1,0 +1,209 @@
+"""MI355X (gfx950) chunkwise delta-rule linear-attention prefill: GDN and KDA.
+
+Thin Python binding over the C ABI of ``include/hagdn.h`` (``libhagdn.so``,
+built in-tree by ``paper_2609_32114_amd.build``).  This module only marshals
+arguments: it allocates outputs and the workspace with torch, passes raw device
+pointers and torch's current HIP stream, and raises on a non-OK status.  Every
+step of the computation runs in the library's HIP kernels; there is no CPU or
+PyTorch fallback, and calls fail loudly when the library is missing.
+
+    o, s_final = gdn_prefill(q, k, v, g, beta, initial_state=None,
+                             cu_seqlens=None, scale=1.0)
+
+Layouts: q, k [T, Hqk, Dk]; v [T, Hv, Dv] (bf16 or fp32, all the same dtype);
+g [T, Hv] fp32 (KDA: [T, Hv, Dk]); beta [T, Hv] fp32; initial_state
+[N, Hv, Dk, Dv] fp32; cu_seqlens int32 [N+1] on the device (None: one
+sequence of length T).  Returns o [T, Hv, Dv] in the input dtype and the final
+state [N, Hv, Dk, Dv] fp32.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+__all__ = ["gdn_prefill", "kda_prefill", "workspace_size", "device_status", "library_path",
+           "load_library", "profile_begin", "profile_end", "kernel_names", "HagdnError"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libhagdn.so")
+_lib = None
+
+HAGDN_F32, HAGDN_BF16 = 0, 1
+DEV_OK, DEV_BAD_SEQLENS = 0, 1
+
+_SYMBOLS = {
+    # name: (restype, argtypes)
+    "gdn_prefill_workspace_size": (ctypes.c_size_t, [ctypes.c_int] * 7),
+    "kda_prefill_workspace_size": (ctypes.c_size_t, [ctypes.c_int] * 7),
+    "gdn_prefill": (ctypes.c_int, [ctypes.c_void_p] * 7 + [ctypes.c_int] * 6 +
+                    [ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "kda_prefill": (ctypes.c_int, [ctypes.c_void_p] * 7 + [ctypes.c_int] * 6 +
+                    [ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "hagdn_last_error": (ctypes.c_char_p, []),
+    "hagdn_device_status": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                           ctypes.POINTER(ctypes.c_int)]),
+    "hagdn_profile_begin": (ctypes.c_int, [ctypes.c_int]),
+    "hagdn_profile_end": (ctypes.c_int, [ctypes.POINTER(ctypes.c_double), ctypes.c_int,
+                                         ctypes.POINTER(ctypes.c_int)]),
+    "hagdn_kernel_count": (ctypes.c_int, []),
+    "hagdn_kernel_name": (ctypes.c_char_p, [ctypes.c_int]),
+    "hagdn_version": (ctypes.c_int, []),
+}
+
+
+class HagdnError(RuntimeError):
+    """A non-OK status from the library (message from hagdn_last_error)."""
+
+    def __init__(self, code, msg):
+        super().__init__(f"hagdn status {code}: {msg}")
+        self.code = code
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libhagdn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2609_32114_amd.build`")
+        lib = ctypes.CDLL(_LIB_PATH)
+        for name, (res, args) in _SYMBOLS.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def _err(lib):
+    m = lib.hagdn_last_error()
+    return m.decode() if m else ""
+
+
+def _dtype_code(t):
+    import torch
+    if t == torch.bfloat16:
+        return HAGDN_BF16
+    if t == torch.float32:
+        return HAGDN_F32
+    raise TypeError(f"unsupported dtype {t}; use torch.bfloat16 or torch.float32")
+
+
+def workspace_size(kind, N, T, Hqk, Hv, Dk, Dv, dtype_code) -> int:
+    lib = load_library()
+    fn = lib.gdn_prefill_workspace_size if kind == "gdn" else lib.kda_prefill_workspace_size
+    n = fn(N, T, Hqk, Hv, Dk, Dv, dtype_code)
+    if n == 0:
+        raise HagdnError(1, _err(lib))
+    return int(n)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _prefill(kind, q, k, v, g, beta, initial_state, cu_seqlens, scale, output_final_state,
+             workspace, out, final_out):
+    import torch
+    lib = load_library()
+    if not (q.is_cuda and k.is_cuda and v.is_cuda and g.is_cuda and beta.is_cuda):
+        raise ValueError("all tensors must be on the GPU")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k, v must share one dtype")
+    dt = _dtype_code(q.dtype)
+    if g.dtype != torch.float32 or beta.dtype != torch.float32:
+        raise TypeError("g and beta must be float32")
+    for name, t in (("q", q), ("k", k), ("v", v), ("g", g), ("beta", beta)):
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    T, Hqk, Dk = q.shape
+    Hv, Dv = v.shape[1], v.shape[2]
+    if k.shape != q.shape or v.shape[0] != T:
+        raise ValueError("shape mismatch between q, k, v")
+    gshape = (T, Hv) if kind == "gdn" else (T, Hv, Dk)
+    if tuple(g.shape) != gshape or tuple(beta.shape) != (T, Hv):
+        raise ValueError(f"g must be {gshape} and beta {(T, Hv)}")
+    dev = q.device
+    if cu_seqlens is None:
+        cu_seqlens = torch.tensor([0, T], dtype=torch.int32, device=dev)
+    if cu_seqlens.dtype != torch.int32 or not cu_seqlens.is_cuda or not cu_seqlens.is_contiguous():
+        raise TypeError("cu_seqlens must be a contiguous int32 GPU tensor")
+    N = cu_seqlens.shape[0] - 1
+    if initial_state is not None:
+        if initial_state.dtype != torch.float32 or tuple(initial_state.shape) != (N, Hv, Dk, Dv) \
+                or not initial_state.is_contiguous():
+            raise ValueError(f"initial_state must be contiguous float32 {(N, Hv, Dk, Dv)}")
+    o = out if out is not None else torch.empty((T, Hv, Dv), dtype=q.dtype, device=dev)
+    sf = None
+    if output_final_state:
+        sf = final_out if final_out is not None else torch.empty((N, Hv, Dk, Dv),
+                                                                 dtype=torch.float32, device=dev)
+    need = workspace_size(kind, N, T, Hqk, Hv, Dk, Dv, dt)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    fn = lib.gdn_prefill if kind == "gdn" else lib.kda_prefill
+    rc = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(initial_state), _ptr(cu_seqlens),
+            N, T, Hqk, Hv, Dk, Dv, float(scale), dt, _ptr(o), _ptr(sf), _ptr(workspace),
+            workspace.numel() * workspace.element_size(), ctypes.c_void_p(stream))
+    if rc != 0:
+        raise HagdnError(rc, _err(lib))
+    return o, sf
+
+
+def gdn_prefill(q, k, v, g, beta, initial_state=None, cu_seqlens=None, scale=1.0,
+                output_final_state=True, workspace=None, out=None, final_out=None):
+    """Gated DeltaNet prefill.  Returns (o, final_state or None)."""
+    return _prefill("gdn", q, k, v, g, beta, initial_state, cu_seqlens, scale, output_final_state,
+                    workspace, out, final_out)
+
+
+def kda_prefill(q, k, v, g, beta, initial_state=None, cu_seqlens=None, scale=1.0,
+                output_final_state=True, workspace=None, out=None, final_out=None):
+    """KDA prefill (per-key-channel log-gate g [T, Hv, Dk]).  Returns (o, final_state or None)."""
+    return _prefill("kda", q, k, v, g, beta, initial_state, cu_seqlens, scale, output_final_state,
+                    workspace, out, final_out)
+
+
+def device_status(workspace) -> int:
+    """Device status word of the last call that used ``workspace`` (synchronises)."""
+    import torch
+    lib = load_library()
+    code = ctypes.c_int(-1)
+    stream = torch.cuda.current_stream(workspace.device).cuda_stream
+    rc = lib.hagdn_device_status(_ptr(workspace), workspace.numel(), ctypes.c_void_p(stream),
+                                 ctypes.byref(code))
+    if rc != 0:
+        raise HagdnError(rc, _err(lib))
+    return code.value
+
+
+def kernel_names():
+    lib = load_library()
+    return [lib.hagdn_kernel_name(i).decode() for i in range(lib.hagdn_kernel_count())]
+
+
+def profile_begin(max_calls: int):
+    lib = load_library()
+    rc = lib.hagdn_profile_begin(int(max_calls))
+    if rc != 0:
+        raise HagdnError(rc, _err(lib))
+
+
+def profile_end():
+    """Returns ({kernel name: mean ms}, calls timed)."""
+    lib = load_library()
+    n = lib.hagdn_kernel_count()
+    arr = (ctypes.c_double * n)()
+    calls = ctypes.c_int(0)
+    rc = lib.hagdn_profile_end(arr, n, ctypes.byref(calls))
+    if rc != 0:
+        raise HagdnError(rc, _err(lib))
+    return dict(zip(kernel_names(), list(arr))), calls.value

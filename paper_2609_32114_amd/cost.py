@@ -35,3 +35,31 @@ def algorithmic_bytes(T_total: int, N: int, Hqk: int, Hv: int, dk: int, dv: int,
     per_token += Hv * 4 * (dk if kda else 1) + Hv * 4              # gate, beta
     state = N * Hv * dk * dv * 4
     return per_token * T_total + state * (2 if with_s0 else 1)
+
+
+def kernel_bytes(kernel: str, T_total: int, N: int, Hqk: int, Hv: int, dk: int, dv: int,
+                 elt_bytes: int, kda: bool, with_s0: bool, chunk: int = 64) -> int:
+    """Compulsory bytes of one kernel of the three-phase pipeline: every input it
+    reads and every output it writes, each counted once.  Per-chunk intermediates
+    are counted over the padded token count (whole 64-token chunks per sequence
+    bounded by T/64 + N chunks; for one full-length sequence this is T)."""
+    e = elt_bytes
+    Tp = T_total  # single sequences with T % 64 == 0 (the timed workloads) have no padding
+    chunks = (T_total + chunk - 1) // chunk
+    gate = Hv * 4 * (dk if kda else 1)
+    state = N * Hv * dk * dv * 4
+    if kernel == "chunk_index":
+        return (N + 1) * 4 + N * 16 + (T_total // chunk + N) * 16 + 4
+    if kernel == "chunk_local":
+        rd = T_total * (2 * Hqk * dk * e + Hv * dv * e + gate + Hv * 4)
+        wr = Tp * Hv * (dk + dv + dk + dk + chunk) * e + chunks * Hv * (dk if kda else 1) * 4
+        return rd + wr
+    if kernel == "state_prop":
+        rd = Tp * Hv * (dk + dv + dk) * e + chunks * Hv * (dk if kda else 1) * 4
+        wr = Tp * Hv * dv * e + chunks * Hv * dk * dv * e
+        return rd + wr + state * (2 if with_s0 else 1)
+    if kernel == "output":
+        rd = chunks * Hv * dk * dv * e + Tp * Hv * (dk + dv + chunk) * e
+        wr = T_total * Hv * dv * e
+        return rd + wr
+    raise KeyError(kernel)

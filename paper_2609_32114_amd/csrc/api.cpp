@@ -1,0 +1,279 @@
+// api.cpp -- the C ABI of include/hagdn.h: host-side argument checks,
+// workspace carving and the four launches, all on the caller's stream.
+//
+// One call enqueues, in stream order:
+//   K0 chunk index   (1 workgroup)                  sequence/chunk tables + cu_seqlens check
+//   K1 chunk-local   (max_chunks x Hv workgroups)   operators #1-#4
+//   K2 state prop    (N x Hv x Dv/16 waves)         operator #5 (sequential over chunks)
+//   K3 output        (max_chunks x Hv workgroups)   operator #6
+// No allocation, no synchronisation, no pointer retained after return.
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/hagdn.h"
+#include "prefill.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+constexpr size_t kAlign = 256;
+constexpr int kNumKernels = 4;
+const char *const kKernelNames[kNumKernels] = {"chunk_index", "chunk_local", "state_prop",
+                                               "output"};
+
+bool mul_ok(size_t a, size_t b, size_t *out) { return !__builtin_mul_overflow(a, b, out); }
+bool add_ok(size_t a, size_t b, size_t *out) { return !__builtin_add_overflow(a, b, out); }
+
+// Byte offsets of every workspace region (each 256-byte aligned).
+struct Layout {
+  size_t status, seq_info, chunk_info, W, Ut, Kt, Qt, P, dec, U, Hs, total;
+  int max_chunks;
+};
+
+// Returns false (with the error set) if the sizes overflow.
+bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, Layout *L) {
+  const size_t mc = (size_t)(T / hagdn::kChunk) + (size_t)N;
+  if (mc > 0x7fffffffu) {
+    fail(HAGDN_EINVAL, "too many chunks (%zu)", mc);
+    return false;
+  }
+  L->max_chunks = (int)mc;
+  size_t blocks;  // (chunk, value head) blocks
+  if (!mul_ok(mc, (size_t)Hv, &blocks)) {
+    fail(HAGDN_EINVAL, "workspace size overflows");
+    return false;
+  }
+  size_t off = 0;
+  bool ok = true;
+  auto region = [&](size_t elems_per_block, size_t bytes_per_elem, size_t nblocks) {
+    size_t at = (off + kAlign - 1) / kAlign * kAlign;
+    size_t b = 0;
+    ok = ok && mul_ok(elems_per_block, bytes_per_elem, &b) && mul_ok(b, nblocks, &b) &&
+         add_ok(at, b, &off);
+    return at;
+  };
+  const size_t C = hagdn::kChunk;
+  L->status = region(1, sizeof(int), 1);
+  L->seq_info = region(1, sizeof(int4), (size_t)N);
+  L->chunk_info = region(1, sizeof(int4), mc);
+  L->W = region(C * Dk, esz, blocks);
+  L->Ut = region((size_t)Dv * C, esz, blocks);
+  L->Kt = region((size_t)Dk * C, esz, blocks);
+  L->Qt = region(C * Dk, esz, blocks);
+  L->P = region(C * C, esz, blocks);
+  L->dec = region((size_t)Dk, sizeof(float), blocks);
+  L->U = region((size_t)Dv * C, esz, blocks);
+  L->Hs = region((size_t)Dv * Dk, esz, blocks);
+  L->total = (off + kAlign - 1) / kAlign * kAlign;
+  if (!ok) fail(HAGDN_EINVAL, "workspace size overflows");
+  return ok;
+}
+
+int check_shapes(int N, int T, int Hqk, int Hv, int Dk, int Dv, int dtype) {
+  if (N < 1) return fail(HAGDN_EINVAL, "N must be >= 1 (got %d)", N);
+  if (T < 0) return fail(HAGDN_EINVAL, "T_total must be >= 0 (got %d)", T);
+  if (Hqk < 1 || Hv < 1) return fail(HAGDN_EINVAL, "head counts must be >= 1 (Hqk=%d Hv=%d)", Hqk, Hv);
+  if (Hv % Hqk != 0) return fail(HAGDN_EINVAL, "Hv (%d) must be a multiple of Hqk (%d)", Hv, Hqk);
+  if (Hv > 65535) return fail(HAGDN_EUNSUPPORTED, "Hv > 65535 unsupported");
+  if ((Dk != 64 && Dk != 128) || (Dv != 64 && Dv != 128))
+    return fail(HAGDN_EUNSUPPORTED, "head dims must be 64 or 128 (Dk=%d Dv=%d)", Dk, Dv);
+  if (dtype != HAGDN_F32 && dtype != HAGDN_BF16)
+    return fail(HAGDN_EUNSUPPORTED, "dtype %d unsupported", dtype);
+  return HAGDN_OK;
+}
+
+size_t workspace_size(int N, int T, int Hqk, int Hv, int Dk, int Dv, int dtype) {
+  if (check_shapes(N, T, Hqk, Hv, Dk, Dv, dtype) != HAGDN_OK) return 0;
+  Layout L;
+  if (!make_layout(N, T, Hv, Dk, Dv, dtype == HAGDN_BF16 ? 2 : 4, &L)) return 0;
+  return L.total;
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// ------------------------------------------------------------------ profiling
+struct Profile {
+  bool on = false;
+  int max_calls = 0;
+  int calls = 0;
+  std::vector<hipEvent_t> ev;  // [max_calls][kNumKernels + 1]
+};
+thread_local Profile g_prof;
+
+void prof_release() {
+  for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
+  g_prof.ev.clear();
+  g_prof.on = false;
+  g_prof.calls = g_prof.max_calls = 0;
+}
+
+int prefill(bool kda, const void *q, const void *k, const void *v, const float *g,
+            const float *beta, const float *s0, const int32_t *cu, int N, int T, int Hqk, int Hv,
+            int Dk, int Dv, float scale, int dtype, void *o, float *s_final, void *ws,
+            size_t ws_bytes, void *stream_) {
+  int rc = check_shapes(N, T, Hqk, Hv, Dk, Dv, dtype);
+  if (rc != HAGDN_OK) return rc;
+  if (!cu || !ws) return fail(HAGDN_EINVAL, "NULL required pointer (cu_seqlens, workspace)");
+  // token tensors are never dereferenced for an empty batch (torch hands out
+  // NULL for zero-size allocations)
+  if (T > 0 && (!q || !k || !v || !g || !beta || !o))
+    return fail(HAGDN_EINVAL, "NULL required pointer (q, k, v, g, beta, o)");
+  const void *p16[] = {q, k, v, o, s0, s_final, ws};
+  const char *n16[] = {"q", "k", "v", "o", "s0", "s_final", "workspace"};
+  for (int i = 0; i < 7; ++i)
+    if (p16[i] && !aligned(p16[i], 16)) return fail(HAGDN_EINVAL, "%s is not 16-byte aligned", n16[i]);
+  if (!aligned(g, 4) || !aligned(beta, 4) || !aligned(cu, 4))
+    return fail(HAGDN_EINVAL, "g, beta and cu_seqlens must be 4-byte aligned");
+  if (s_final && s0 && s_final != s0) {
+    const size_t sb = (size_t)N * Hv * Dk * Dv * sizeof(float);
+    const char *a0 = (const char *)s0, *a1 = (const char *)s_final;
+    if (a0 < a1 + sb && a1 < a0 + sb) return fail(HAGDN_EINVAL, "s_final overlaps s0 without aliasing it exactly");
+  }
+  const bool bf16 = dtype == HAGDN_BF16;
+  Layout L;
+  if (!make_layout(N, T, Hv, Dk, Dv, bf16 ? 2 : 4, &L)) return HAGDN_EINVAL;
+  if (ws_bytes < L.total)
+    return fail(HAGDN_EWORKSPACE, "workspace too small: %zu bytes given, %zu needed", ws_bytes, L.total);
+
+  char *w = static_cast<char *>(ws);
+  hagdn::PrefillArgs a;
+  a.q = q; a.k = k; a.v = v; a.g = g; a.beta = beta; a.s0 = s0; a.cu_seqlens = cu;
+  a.N = N; a.T = T; a.Hqk = Hqk; a.Hv = Hv; a.Dk = Dk; a.Dv = Dv;
+  a.max_chunks = L.max_chunks;
+  a.scale = scale;
+  a.o = o; a.s_final = s_final;
+  a.status = reinterpret_cast<int *>(w + L.status);
+  a.seq_info = reinterpret_cast<int4 *>(w + L.seq_info);
+  a.chunk_info = reinterpret_cast<int4 *>(w + L.chunk_info);
+  a.W = w + L.W; a.Ut = w + L.Ut; a.Kt = w + L.Kt; a.Qt = w + L.Qt; a.P = w + L.P;
+  a.dec = reinterpret_cast<float *>(w + L.dec);
+  a.U = w + L.U; a.Hs = w + L.Hs;
+
+  hipStream_t st = static_cast<hipStream_t>(stream_);
+  hipEvent_t *ev = nullptr;
+  if (g_prof.on && g_prof.calls < g_prof.max_calls)
+    ev = &g_prof.ev[(size_t)g_prof.calls++ * (kNumKernels + 1)];
+  auto mark = [&](int i) -> hipError_t { return ev ? hipEventRecord(ev[i], st) : hipSuccess; };
+
+  hipError_t e;
+  if ((e = mark(0)) != hipSuccess) goto hip_fail;
+  if ((e = hagdn::launch_chunk_index(a, st)) != hipSuccess) goto hip_fail;
+  if ((e = mark(1)) != hipSuccess) goto hip_fail;
+  if ((e = hagdn::launch_chunk_local(a, bf16, kda, st)) != hipSuccess) goto hip_fail;
+  if ((e = mark(2)) != hipSuccess) goto hip_fail;
+  if ((e = hagdn::launch_state_prop(a, bf16, kda, st)) != hipSuccess) goto hip_fail;
+  if ((e = mark(3)) != hipSuccess) goto hip_fail;
+  if ((e = hagdn::launch_output(a, bf16, st)) != hipSuccess) goto hip_fail;
+  if ((e = mark(4)) != hipSuccess) goto hip_fail;
+  return HAGDN_OK;
+hip_fail:
+  return fail(HAGDN_EHIP, "HIP error: %s", hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t gdn_prefill_workspace_size(int N, int T_total, int Hqk, int Hv, int Dk, int Dv, int dtype) {
+  return workspace_size(N, T_total, Hqk, Hv, Dk, Dv, dtype);
+}
+
+size_t kda_prefill_workspace_size(int N, int T_total, int Hqk, int Hv, int Dk, int Dv, int dtype) {
+  return workspace_size(N, T_total, Hqk, Hv, Dk, Dv, dtype);
+}
+
+int gdn_prefill(const void *q, const void *k, const void *v, const float *g, const float *beta,
+                const float *s0, const int32_t *cu_seqlens, int N, int T_total, int Hqk, int Hv,
+                int Dk, int Dv, float scale, int dtype, void *o, float *s_final, void *workspace,
+                size_t workspace_bytes, void *stream) {
+  return prefill(false, q, k, v, g, beta, s0, cu_seqlens, N, T_total, Hqk, Hv, Dk, Dv, scale,
+                 dtype, o, s_final, workspace, workspace_bytes, stream);
+}
+
+int kda_prefill(const void *q, const void *k, const void *v, const float *g, const float *beta,
+                const float *s0, const int32_t *cu_seqlens, int N, int T_total, int Hqk, int Hv,
+                int Dk, int Dv, float scale, int dtype, void *o, float *s_final, void *workspace,
+                size_t workspace_bytes, void *stream) {
+  return prefill(true, q, k, v, g, beta, s0, cu_seqlens, N, T_total, Hqk, Hv, Dk, Dv, scale,
+                 dtype, o, s_final, workspace, workspace_bytes, stream);
+}
+
+const char *hagdn_last_error(void) { return g_err.c_str(); }
+
+int hagdn_device_status(const void *workspace, size_t workspace_bytes, void *stream, int *code) {
+  if (!workspace || !code) return fail(HAGDN_EINVAL, "NULL workspace or code");
+  if (workspace_bytes < sizeof(int)) return fail(HAGDN_EINVAL, "workspace too small");
+  int host = -1;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(&host, workspace, sizeof(int), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return fail(HAGDN_EHIP, "HIP error: %s", hipGetErrorString(e));
+  *code = host;
+  return HAGDN_OK;
+}
+
+int hagdn_profile_begin(int max_calls) {
+  if (max_calls < 1 || max_calls > (1 << 20)) return fail(HAGDN_EINVAL, "max_calls out of range");
+  prof_release();
+  g_prof.ev.assign((size_t)max_calls * (kNumKernels + 1), nullptr);
+  for (hipEvent_t &e : g_prof.ev) {
+    hipError_t r = hipEventCreate(&e);
+    if (r != hipSuccess) {
+      prof_release();
+      return fail(HAGDN_EHIP, "hipEventCreate: %s", hipGetErrorString(r));
+    }
+  }
+  g_prof.max_calls = max_calls;
+  g_prof.calls = 0;
+  g_prof.on = true;
+  return HAGDN_OK;
+}
+
+int hagdn_profile_end(double *mean_ms, int max_kernels, int *calls) {
+  if (!g_prof.on) return fail(HAGDN_EINVAL, "profiling was not started");
+  const int nc = g_prof.calls;
+  std::vector<double> sum(kNumKernels, 0.0);
+  for (int c = 0; c < nc; ++c) {
+    hipEvent_t *ev = &g_prof.ev[(size_t)c * (kNumKernels + 1)];
+    hipError_t r = hipEventSynchronize(ev[kNumKernels]);
+    for (int i = 0; i < kNumKernels && r == hipSuccess; ++i) {
+      float ms = 0.f;
+      r = hipEventElapsedTime(&ms, ev[i], ev[i + 1]);
+      sum[i] += ms;
+    }
+    if (r != hipSuccess) {
+      prof_release();
+      return fail(HAGDN_EHIP, "event timing: %s", hipGetErrorString(r));
+    }
+  }
+  for (int i = 0; i < kNumKernels && i < max_kernels && mean_ms; ++i)
+    mean_ms[i] = nc ? sum[i] / nc : 0.0;
+  if (calls) *calls = nc;
+  prof_release();
+  return HAGDN_OK;
+}
+
+int hagdn_kernel_count(void) { return kNumKernels; }
+
+const char *hagdn_kernel_name(int i) { return (i >= 0 && i < kNumKernels) ? kKernelNames[i] : ""; }
+
+int hagdn_version(void) { return 100; }
+
+}  // extern "C"

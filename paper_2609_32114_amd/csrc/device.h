@@ -1,0 +1,187 @@
+// device.h -- CDNA4 (gfx950) building blocks shared by the prefill kernels:
+// 16x16 MFMA tiles for bf16 and fp32 operands, the lane layout of their
+// fragments, and conversions.
+//
+// Tile conventions (one wave64, 16x16 output tile D = A B + C):
+//   * accumulator: lane l holds column (l & 15), rows 4*(l >> 4) + e, e = 0..3
+//     (an f32x4);
+//   * operand fragments cover a k-block of 32: lane l feeds row (A) or column
+//     (B) (l & 15) with 8 values.  Value j of lane group grp = l >> 4 carries
+//     logical k index
+//         kmap(grp, j) = 4*grp + j          for j < 4
+//                        16 + 4*grp + j - 4 for j >= 4.
+//     A and B use the same map, so the contraction pairs the right values
+//     whatever order the hardware assigns to the 8 slots of a lane.
+//   * with this map an accumulator pair (rows 0-15 tile, rows 16-31 tile) IS
+//     the B fragment of a k-block over those 32 rows, lane for lane: a result
+//     can feed the next product without any cross-lane movement.  The state
+//     chain of the sequential kernel relies on this.
+//   * a fragment read from memory whose k index is contiguous takes two runs
+//     of 4 elements: [k0 + 4*grp, +4) and [k0 + 16 + 4*grp, +4).
+// bf16 operands use v_mfma_f32_16x16x32_bf16 (one instruction per k-block);
+// fp32 operands use v_mfma_f32_16x16x4_f32 (eight instructions per k-block,
+// step j contracting the four values j of the four lane groups).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hagdn {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t bf16_t;  // bf16 storage
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+// --------------------------------------------------------------- conversions
+__device__ __forceinline__ float bf16_to_f32(bf16_t x) {
+  return __uint_as_float(((uint32_t)x) << 16);
+}
+// Round to nearest even (the hardware conversion on gfx950).
+__device__ __forceinline__ bf16_t f32_to_bf16(float x) {
+  __bf16 b = (__bf16)x;
+  return __builtin_bit_cast(bf16_t, b);
+}
+
+template <typename T> struct Elt;
+template <> struct Elt<bf16_t> {
+  using frag = bf16x8;
+  __device__ static float to_f32(bf16_t x) { return bf16_to_f32(x); }
+  __device__ static bf16_t from_f32(float x) { return f32_to_bf16(x); }
+};
+template <> struct Elt<float> {
+  using frag = f32x8;
+  __device__ static float to_f32(float x) { return x; }
+  __device__ static float from_f32(float x) { return x; }
+};
+
+template <typename T> using Frag = typename Elt<T>::frag;
+
+// logical k index of value j held by lane group grp (see header comment)
+__device__ __forceinline__ constexpr int kmap(int grp, int j) {
+  return j < 4 ? 4 * grp + j : 12 + 4 * grp + j;
+}
+
+// ------------------------------------------------------------ 4-element I/O
+// Four consecutive elements as fp32 (8-byte load for bf16, 16-byte for fp32).
+__device__ __forceinline__ f32x4 load4(const bf16_t *p) {
+  uint2 u = *reinterpret_cast<const uint2 *>(p);
+  f32x4 r;
+  r[0] = __uint_as_float(u.x << 16);
+  r[1] = __uint_as_float(u.x & 0xffff0000u);
+  r[2] = __uint_as_float(u.y << 16);
+  r[3] = __uint_as_float(u.y & 0xffff0000u);
+  return r;
+}
+__device__ __forceinline__ f32x4 load4(const float *p) {
+  return *reinterpret_cast<const f32x4 *>(p);
+}
+__device__ __forceinline__ void store4(bf16_t *p, f32x4 v) {
+  uint2 u;
+  u.x = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+  u.y = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+  *reinterpret_cast<uint2 *>(p) = u;
+}
+__device__ __forceinline__ void store4(float *p, f32x4 v) {
+  *reinterpret_cast<f32x4 *>(p) = v;
+}
+
+// ---------------------------------------------------- 16-byte vector access
+// A uint4 holds 8 bf16 or 4 fp32 elements; element j (compile-time after
+// unrolling) read as fp32, read raw, or packed from fp32 with rounding.
+__device__ __forceinline__ uint32_t word(uint4 u, int i) {
+  return i == 0 ? u.x : i == 1 ? u.y : i == 2 ? u.z : u.w;
+}
+template <typename T> struct Vec16;
+template <> struct Vec16<bf16_t> {
+  static constexpr int N = 8;
+  __device__ static float get(uint4 u, int j) {
+    const uint32_t w = word(u, j >> 1);
+    return __uint_as_float((j & 1) ? (w & 0xffff0000u) : (w << 16));
+  }
+  __device__ static bf16_t raw(uint4 u, int j) {
+    const uint32_t w = word(u, j >> 1);
+    return (bf16_t)((j & 1) ? (w >> 16) : (w & 0xffffu));
+  }
+  __device__ static uint4 pack(const float (&x)[8]) {
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = (uint32_t)f32_to_bf16(x[2 * i]) | ((uint32_t)f32_to_bf16(x[2 * i + 1]) << 16);
+    return make_uint4(w[0], w[1], w[2], w[3]);
+  }
+};
+template <> struct Vec16<float> {
+  static constexpr int N = 4;
+  __device__ static float get(uint4 u, int j) { return __uint_as_float(word(u, j)); }
+  __device__ static float raw(uint4 u, int j) { return __uint_as_float(word(u, j)); }
+  __device__ static uint4 pack(const float (&x)[4]) {
+    return make_uint4(__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]),
+                      __float_as_uint(x[3]));
+  }
+};
+
+// ------------------------------------------------------------- fragments
+// Fragment from memory with contiguous k: row/column pointer at the k-block base.
+__device__ __forceinline__ bf16x8 load_frag(const bf16_t *p, int grp) {
+  uint2 a = *reinterpret_cast<const uint2 *>(p + 4 * grp);
+  uint2 b = *reinterpret_cast<const uint2 *>(p + 16 + 4 * grp);
+  uint4 u = make_uint4(a.x, a.y, b.x, b.y);
+  return __builtin_bit_cast(bf16x8, u);
+}
+__device__ __forceinline__ f32x8 load_frag(const float *p, int grp) {
+  f32x4 a = *reinterpret_cast<const f32x4 *>(p + 4 * grp);
+  f32x4 b = *reinterpret_cast<const f32x4 *>(p + 16 + 4 * grp);
+  f32x8 r;
+  r[0] = a[0]; r[1] = a[1]; r[2] = a[2]; r[3] = a[3];
+  r[4] = b[0]; r[5] = b[1]; r[6] = b[2]; r[7] = b[3];
+  return r;
+}
+
+// Fragment from eight fp32 values (in kmap order), rounded to the operand type.
+template <typename T> __device__ __forceinline__ Frag<T> make_frag(const float (&x)[8]);
+template <> __device__ __forceinline__ bf16x8 make_frag<bf16_t>(const float (&x)[8]) {
+  bf16x8 r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = (__bf16)x[j];
+  return r;
+}
+template <> __device__ __forceinline__ f32x8 make_frag<float>(const float (&x)[8]) {
+  f32x8 r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = x[j];
+  return r;
+}
+
+// B fragment over 32 rows from two accumulator tiles (rows 0-15, rows 16-31),
+// each value multiplied by `mul` before rounding.
+template <typename T>
+__device__ __forceinline__ Frag<T> frag_from_acc(f32x4 lo, f32x4 hi, float mul) {
+  float x[8] = {lo[0] * mul, lo[1] * mul, lo[2] * mul, lo[3] * mul,
+                hi[0] * mul, hi[1] * mul, hi[2] * mul, hi[3] * mul};
+  return make_frag<T>(x);
+}
+
+template <typename T> __device__ __forceinline__ Frag<T> zero_frag() {
+  float x[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  return make_frag<T>(x);
+}
+
+// --------------------------------------------------------------------- MFMA
+__device__ __forceinline__ f32x4 mma(f32x4 acc, bf16x8 a, bf16x8 b) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma(f32x4 acc, f32x8 a, f32x8 b) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[j], b[j], acc, 0, 0, 0);
+  return acc;
+}
+
+__device__ __forceinline__ f32x4 zero4() {
+  f32x4 z = {0.f, 0.f, 0.f, 0.f};
+  return z;
+}
+
+}  // namespace hagdn

@@ -1,0 +1,98 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+public header declares, sizes workspaces, and rejects bad arguments on the
+host before anything is enqueued (fake, never-dereferenced device pointers)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_32114_amd as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hagdn.h")
+
+needs_lib = pytest.mark.skipif(not os.path.exists(P.library_path()),
+                               reason="libhagdn.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("gdn_prefill", "kda_prefill", "gdn_prefill_workspace_size",
+              "kda_prefill_workspace_size", "hagdn_last_error", "hagdn_device_status"):
+        assert n in names
+
+
+@needs_lib
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(P.library_path())
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+@needs_lib
+def test_workspace_size():
+    n1 = P.workspace_size("gdn", 1, 4096, 16, 16, 128, 128, P.HAGDN_BF16)
+    n2 = P.workspace_size("gdn", 1, 4096, 16, 16, 128, 128, P.HAGDN_F32)
+    assert n1 > 0 and n2 > n1
+    assert P.workspace_size("kda", 1, 0, 1, 1, 64, 64, P.HAGDN_F32) > 0
+    for bad in [(0, 64, 1, 1, 64, 64, 1), (1, 64, 2, 3, 64, 64, 1), (1, 64, 1, 1, 96, 64, 1),
+                (1, 64, 1, 1, 64, 64, 7), (1, -1, 1, 1, 64, 64, 1)]:
+        with pytest.raises(P.HagdnError):
+            P.workspace_size("gdn", *bad)
+
+
+FAKE = 0x100000  # 16-byte aligned, never dereferenced
+
+
+def _call(lib, kind="gdn", N=1, T=100, Hqk=1, Hv=1, Dk=64, Dv=64, dtype=0, ws_bytes=1 << 40,
+          **over):
+    ptrs = dict(q=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE, s0=None, cu=FAKE, o=FAKE, sf=None,
+                ws=FAKE)
+    ptrs.update(over)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    fn = lib.gdn_prefill if kind == "gdn" else lib.kda_prefill
+    rc = fn(vp(ptrs["q"]), vp(ptrs["k"]), vp(ptrs["v"]), vp(ptrs["g"]), vp(ptrs["beta"]),
+            vp(ptrs["s0"]), vp(ptrs["cu"]), N, T, Hqk, Hv, Dk, Dv, 1.0, dtype, vp(ptrs["o"]),
+            vp(ptrs["sf"]), vp(ptrs["ws"]), ws_bytes, None)
+    return rc, lib.hagdn_last_error().decode()
+
+
+@needs_lib
+@pytest.mark.parametrize("kind", ["gdn", "kda"])
+def test_host_validation(kind):
+    lib = P.load_library()
+    EINVAL, EUNSUP, EWS = 1, 2, 3
+    assert _call(lib, kind, q=None)[0] == EINVAL
+    assert _call(lib, kind, o=None)[0] == EINVAL
+    assert _call(lib, kind, cu=None)[0] == EINVAL
+    assert _call(lib, kind, ws=None)[0] == EINVAL
+    assert _call(lib, kind, N=0)[0] == EINVAL
+    assert _call(lib, kind, T=-5)[0] == EINVAL
+    assert _call(lib, kind, Hqk=2, Hv=3)[0] == EINVAL
+    assert _call(lib, kind, Dk=32)[0] == EUNSUP
+    assert _call(lib, kind, Dv=256)[0] == EUNSUP
+    assert _call(lib, kind, dtype=2)[0] == EUNSUP
+    assert _call(lib, kind, q=FAKE + 8)[0] == EINVAL            # misaligned
+    assert _call(lib, kind, s0=FAKE + 4, sf=FAKE + 4)[0] == EINVAL
+    assert _call(lib, kind, g=FAKE + 2)[0] == EINVAL
+    rc, msg = _call(lib, kind, ws_bytes=64)
+    assert rc == EWS and "workspace too small" in msg
+    # s_final overlapping s0 without aliasing it exactly
+    assert _call(lib, kind, s0=FAKE, sf=FAKE + 64)[0] == EINVAL
+
+
+@needs_lib
+def test_profile_requires_begin():
+    lib = P.load_library()
+    arr = (ctypes.c_double * 4)()
+    calls = ctypes.c_int()
+    assert lib.hagdn_profile_end(arr, 4, ctypes.byref(calls)) == 1
+    assert lib.hagdn_profile_begin(0) == 1

@@ -1,0 +1,162 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Small cases compare every element and span several 64-token chunks with
+ragged tails; the full-size workloads run in the benchmark's launch
+configuration and compare sampled heads, for which the oracle runs alone
+(every (sequence, head) pair of the method is independent).  Tolerance:
+max|gpu - oracle| / max|oracle| <= 1e-4 (fp32 inputs), <= 2e-2 (bf16 inputs).
+"""
+
+import numpy as np
+import pytest
+
+from gpu_harness import TOL, check_against_oracle, run_gpu, say, to_device
+from paper_2609_32114_amd.inputs import make_case, make_workload
+
+pytestmark = pytest.mark.gpu
+
+
+def test_workload0_full():
+    check_against_oracle(make_workload(0), label="workload0")
+
+
+SMALL = [
+    # kind, lengths, Hqk, Hv, Dk, Dv, dtype, s0
+    ("gdn", (1,), 1, 1, 64, 64, "f32", True),
+    ("gdn", (63,), 1, 2, 64, 64, "f32", True),
+    ("gdn", (65,), 2, 2, 128, 128, "f32", True),
+    ("gdn", (200,), 2, 2, 128, 128, "bf16", True),
+    ("gdn", (130,), 1, 1, 64, 128, "bf16", False),
+    ("gdn", (130,), 1, 1, 128, 64, "f32", True),
+    ("gdn", (129,), 2, 4, 128, 128, "bf16", True),
+    ("kda", (1,), 1, 1, 64, 64, "f32", True),
+    ("kda", (200,), 1, 2, 64, 64, "f32", True),
+    ("kda", (200,), 2, 2, 128, 128, "bf16", True),
+    ("kda", (130,), 1, 2, 128, 64, "bf16", False),
+    ("kda", (97,), 2, 4, 64, 128, "f32", True),
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=lambda c: f"{c[0]}-T{sum(c[1])}-h{c[2]}x{c[3]}-d{c[4]}x{c[5]}-{c[6]}")
+def test_small_shapes(case):
+    kind, lengths, Hqk, Hv, Dk, Dv, dtype, s0 = case
+    inp = make_case(kind, lengths, Hqk, Hv, Dk, Dv, dtype, with_s0=s0, seed=7)
+    check_against_oracle(inp, label="small")
+
+
+@pytest.mark.parametrize("kind", ["gdn", "kda"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_varlen_small(kind, dtype):
+    inp = make_case(kind, (0, 1, 64, 65, 130, 7, 0, 200), 2, 4, 128, 128, dtype, with_s0=True,
+                    seed=11)
+    check_against_oracle(inp, label="varlen")
+
+
+@pytest.mark.parametrize("variant", ["lm", "dn", "ks", "s0", "lg"])
+def test_stress_variants_small(variant):
+    for kind in ("gdn", "kda"):
+        inp = make_case(kind, (300,), 1, 2, 128, 128, "bf16", variant=variant, seed=21)
+        check_against_oracle(inp, label=f"stress-{variant}")
+        inp = make_case(kind, (300,), 1, 2, 64, 64, "f32", variant=variant, seed=22)
+        check_against_oracle(inp, label=f"stress-{variant}")
+
+
+def test_scale_and_inplace_state():
+    import torch
+    import paper_2609_32114_amd as P
+    inp = make_case("gdn", (150,), 1, 2, 128, 128, "bf16", with_s0=True, seed=3,
+                    scale=128 ** -0.5)
+    check_against_oracle(inp, label="scale")
+    d = to_device(inp)
+    o_ref, s_ref = run_gpu(inp)
+    state = d["s0"].clone()
+    o, sf = P.gdn_prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], initial_state=state,
+                          cu_seqlens=d["cu"], scale=inp.scale, final_out=state)
+    torch.cuda.synchronize()
+    assert sf.data_ptr() == state.data_ptr()
+    np.testing.assert_array_equal(state.cpu().numpy(), s_ref.astype(np.float32))
+    np.testing.assert_array_equal(o.float().cpu().numpy(), o_ref.astype(np.float32))
+
+
+def test_no_final_state_and_zero_state():
+    import torch
+    import paper_2609_32114_amd as P
+    inp = make_case("kda", (90,), 1, 1, 64, 64, "f32", seed=4)
+    d = to_device(inp)
+    o, sf = P.kda_prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], cu_seqlens=d["cu"],
+                          output_final_state=False)
+    torch.cuda.synchronize()
+    assert sf is None
+    o_ref, _ = run_gpu(inp)
+    np.testing.assert_array_equal(o.float().cpu().numpy(), o_ref.astype(np.float32))
+
+
+def test_empty_batch_returns_initial_state():
+    import torch
+    import paper_2609_32114_amd as P
+    for kind in ("gdn", "kda"):
+        inp = make_case(kind, (0, 0), 1, 2, 64, 64, "bf16", with_s0=True, seed=5)
+        d = to_device(inp)
+        fn = P.gdn_prefill if kind == "gdn" else P.kda_prefill
+        o, sf = fn(d["q"], d["k"], d["v"], d["g"], d["beta"], initial_state=d["s0"],
+                   cu_seqlens=d["cu"])
+        torch.cuda.synchronize()
+        assert o.shape[0] == 0
+        np.testing.assert_array_equal(sf.cpu().numpy(), inp.s0)
+
+
+def test_bad_seqlens_are_reported_not_faulted():
+    import torch
+    import paper_2609_32114_amd as P
+    inp = make_case("gdn", (100, 50), 1, 1, 64, 64, "f32", with_s0=True, seed=6)
+    d = to_device(inp)
+    ws = torch.zeros(P.workspace_size("gdn", 2, 150, 1, 1, 64, 64, P.HAGDN_F32),
+                     dtype=torch.uint8, device="cuda")
+    for bad in ([0, 120, 100], [5, 100, 150], [0, 100, 149]):   # decreasing, cu[0]!=0, cu[N]!=T
+        cu = torch.tensor(bad, dtype=torch.int32, device="cuda")
+        o = torch.full((150, 1, 64), 7.0, device="cuda")
+        o, sf = P.gdn_prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], initial_state=d["s0"],
+                              cu_seqlens=cu, workspace=ws, out=o)
+        assert P.device_status(ws) == P.DEV_BAD_SEQLENS
+        np.testing.assert_array_equal(sf.cpu().numpy(), inp.s0)
+        assert torch.all(o == 7.0)
+    o, sf = P.gdn_prefill(d["q"], d["k"], d["v"], d["g"], d["beta"], initial_state=d["s0"],
+                          cu_seqlens=d["cu"], workspace=ws)
+    assert P.device_status(ws) == P.DEV_OK
+
+
+def test_bitwise_deterministic():
+    inp = make_case("gdn", (1000, 333), 2, 4, 128, 128, "bf16", with_s0=True, seed=8)
+    d = to_device(inp)
+    a = run_gpu(inp, dev=d)
+    b = run_gpu(inp, dev=d)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+
+
+# ------------------------------------------------------------ full-size workloads
+SAMPLED = {1: [0, 7, 15], 2: [0, 9], 3: [0, 5, 15], 4: [0, 17, 31]}
+
+
+@pytest.mark.parametrize("idx", [1, 2, 3, 4])
+def test_workload_full_size_sampled_heads(idx):
+    inp = make_workload(idx)
+    check_against_oracle(inp, heads=SAMPLED[idx], label=f"workload{idx}")
+
+
+@pytest.mark.parametrize("variant", ["lm", "dn", "ks", "s0"])
+def test_workload1_shape_stress(variant):
+    inp = make_workload(1, variant=variant)
+    check_against_oracle(inp, heads=[3, 12], label=f"workload1-{variant}")
+
+
+@pytest.mark.parametrize("variant", ["lm", "lg"])
+def test_workload3_shape_stress(variant):
+    inp = make_workload(3, variant=variant)
+    check_against_oracle(inp, heads=[2], label=f"workload3-{variant}")
+
+
+@pytest.mark.parametrize("variant", ["dn", "s0"])
+def test_workload2_shape_stress(variant):
+    inp = make_workload(2, variant=variant)
+    check_against_oracle(inp, heads=[4], label=f"workload2-{variant}")
