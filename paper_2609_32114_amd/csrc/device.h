@@ -6,18 +6,21 @@
 //   * accumulator: lane l holds column (l & 15), rows 4*(l >> 4) + e, e = 0..3
 //     (an f32x4);
 //   * operand fragments cover a k-block of 32: lane l feeds row (A) or column
-//     (B) (l & 15) with 8 values.  Value j of lane group grp = l >> 4 carries
-//     logical k index
-//         kmap(grp, j) = 4*grp + j          for j < 4
-//                        16 + 4*grp + j - 4 for j >= 4.
-//     A and B use the same map, so the contraction pairs the right values
-//     whatever order the hardware assigns to the 8 slots of a lane.
-//   * with this map an accumulator pair (rows 0-15 tile, rows 16-31 tile) IS
-//     the B fragment of a k-block over those 32 rows, lane for lane: a result
-//     can feed the next product without any cross-lane movement.  The state
-//     chain of the sequential kernel relies on this.
-//   * a fragment read from memory whose k index is contiguous takes two runs
-//     of 4 elements: [k0 + 4*grp, +4) and [k0 + 16 + 4*grp, +4).
+//     (B) (l & 15) with 8 values; lane group grp = l >> 4 supplies 8 of the 32
+//     k indices.  A and B of one product must agree on which logical k index
+//     each (grp, j) slot carries; the hardware's own slot order never matters.
+//   * two slot maps are used:
+//       contiguous   kc(grp, j) = 8*grp + j            -- both operands read
+//                    from memory: one 16-byte load per lane (load_frag);
+//       accumulator  kmap(grp, j) = 4*grp + j (j < 4), 16 + 4*grp + j - 4 (j >= 4)
+//                    -- the map under which an accumulator pair (rows 0-15
+//                    tile, rows 16-31 tile) IS the B fragment of a k-block over
+//                    those 32 rows, lane for lane (frag_from_acc): a result
+//                    feeds the next product with no cross-lane movement.  The
+//                    partner A operand of such a product is stored
+//                    "kmap-permuted": inside every 32-block, position 8*grp + j
+//                    holds logical index kmap(grp, j).  It is then read with
+//                    the same contiguous 16-byte load_frag.
 // bf16 operands use v_mfma_f32_16x16x32_bf16 (one instruction per k-block);
 // fp32 operands use v_mfma_f32_16x16x4_f32 (eight instructions per k-block,
 // step j contracting the four values j of the four lane groups).
@@ -31,6 +34,9 @@ namespace hagdn {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x8 __attribute__((ext_vector_type(8)));
+// 16 raw bytes as a native vector: unlike HIP's union-based uint4 it stays in
+// registers when held in arrays.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef uint16_t bf16_t;  // bf16 storage
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
@@ -59,9 +65,13 @@ template <> struct Elt<float> {
 
 template <typename T> using Frag = typename Elt<T>::frag;
 
-// logical k index of value j held by lane group grp (see header comment)
+// logical k index of slot j of lane group grp under the accumulator map
 __device__ __forceinline__ constexpr int kmap(int grp, int j) {
   return j < 4 ? 4 * grp + j : 12 + 4 * grp + j;
+}
+// position inside a kmap-permuted 32-block of logical index i (0..31)
+__device__ __forceinline__ constexpr int kmap_pos(int i) {
+  return i < 16 ? 8 * (i >> 2) + (i & 3) : 8 * ((i - 16) >> 2) + 4 + (i & 3);
 }
 
 // ------------------------------------------------------------ 4-element I/O
@@ -124,29 +134,31 @@ template <> struct Vec16<float> {
 };
 
 // ------------------------------------------------------------- fragments
-// Fragment from memory with contiguous k: row/column pointer at the k-block base.
+// Fragment of the 32-block at p: lane group grp reads elements [8*grp, 8*grp + 8)
+// (one 16-byte load for bf16).  Logical order under the contiguous map, or
+// kmap order when the block is stored kmap-permuted.
 __device__ __forceinline__ bf16x8 load_frag(const bf16_t *p, int grp) {
-  uint2 a = *reinterpret_cast<const uint2 *>(p + 4 * grp);
-  uint2 b = *reinterpret_cast<const uint2 *>(p + 16 + 4 * grp);
-  uint4 u = make_uint4(a.x, a.y, b.x, b.y);
-  return __builtin_bit_cast(bf16x8, u);
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(p + 8 * grp));
 }
 __device__ __forceinline__ f32x8 load_frag(const float *p, int grp) {
-  f32x4 a = *reinterpret_cast<const f32x4 *>(p + 4 * grp);
-  f32x4 b = *reinterpret_cast<const f32x4 *>(p + 16 + 4 * grp);
+  f32x4 a = *reinterpret_cast<const f32x4 *>(p + 8 * grp);
+  f32x4 b = *reinterpret_cast<const f32x4 *>(p + 8 * grp + 4);
   f32x8 r;
   r[0] = a[0]; r[1] = a[1]; r[2] = a[2]; r[3] = a[3];
   r[4] = b[0]; r[5] = b[1]; r[6] = b[2]; r[7] = b[3];
   return r;
 }
+// Contiguous-map logical k index of slot j of lane group grp.
+__device__ __forceinline__ constexpr int kc(int grp, int j) { return 8 * grp + j; }
 
 // Fragment from eight fp32 values (in kmap order), rounded to the operand type.
 template <typename T> __device__ __forceinline__ Frag<T> make_frag(const float (&x)[8]);
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 template <> __device__ __forceinline__ bf16x8 make_frag<bf16_t>(const float (&x)[8]) {
-  bf16x8 r;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) r[j] = (__bf16)x[j];
-  return r;
+  // two packed conversions per 4 values (v_cvt_pk_bf16_f32), no repacking
+  const f32x4 lo = {x[0], x[1], x[2], x[3]}, hi = {x[4], x[5], x[6], x[7]};
+  const bf16x4 a = __builtin_convertvector(lo, bf16x4), b = __builtin_convertvector(hi, bf16x4);
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 template <> __device__ __forceinline__ f32x8 make_frag<float>(const float (&x)[8]) {
   f32x8 r;
@@ -155,13 +167,23 @@ template <> __device__ __forceinline__ f32x8 make_frag<float>(const float (&x)[8
   return r;
 }
 
-// B fragment over 32 rows from two accumulator tiles (rows 0-15, rows 16-31),
-// each value multiplied by `mul` before rounding.
-template <typename T>
-__device__ __forceinline__ Frag<T> frag_from_acc(f32x4 lo, f32x4 hi, float mul) {
-  float x[8] = {lo[0] * mul, lo[1] * mul, lo[2] * mul, lo[3] * mul,
-                hi[0] * mul, hi[1] * mul, hi[2] * mul, hi[3] * mul};
-  return make_frag<T>(x);
+// B fragment over 32 rows from two accumulator tiles (rows 0-15, rows 16-31).
+template <typename T> __device__ __forceinline__ Frag<T> frag_from_acc(f32x4 lo, f32x4 hi);
+template <> __device__ __forceinline__ bf16x8 frag_from_acc<bf16_t>(f32x4 lo, f32x4 hi) {
+  const bf16x4 a = __builtin_convertvector(lo, bf16x4), b = __builtin_convertvector(hi, bf16x4);
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+template <> __device__ __forceinline__ f32x8 frag_from_acc<float>(f32x4 lo, f32x4 hi) {
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Store a fragment where load_frag would read it: 8 elements at p + 8*grp.
+__device__ __forceinline__ void store_frag(bf16_t *p, bf16x8 f, int grp) {
+  *reinterpret_cast<uint4 *>(p + 8 * grp) = __builtin_bit_cast(uint4, f);
+}
+__device__ __forceinline__ void store_frag(float *p, f32x8 f, int grp) {
+  *reinterpret_cast<f32x4 *>(p + 8 * grp) = __builtin_shufflevector(f, f, 0, 1, 2, 3);
+  *reinterpret_cast<f32x4 *>(p + 8 * grp + 4) = __builtin_shufflevector(f, f, 4, 5, 6, 7);
 }
 
 template <typename T> __device__ __forceinline__ Frag<T> zero_frag() {

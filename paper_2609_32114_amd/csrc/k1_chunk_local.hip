@@ -12,6 +12,11 @@
 //   #4  W  = T Diag(b) (K * e^gamma)         U~ = T Diag(b) V
 // plus the operands the sequential kernel and the output kernel consume:
 //   Kt = (K * e^(gamma_last - gamma))^T,  Qt = Q * e^gamma,  dec = e^gamma_last.
+// W and Kt are the A operands of the state kernel's chained products and are
+// stored kmap-permuted inside each 32-block (see device.h), W negated; Qt and P
+// are the partners of the state kernel's fragment-order outputs (snapshot,
+// corrected values) in the output kernel and are kmap-permuted along d_k and
+// along tokens respectively.  Ut is stored in logical order.
 // P is the decay-masked Q K^T of Sec. 5's GEMM group (KK^T and QK^T share K
 // and are computed together); the solve never has to wait on a GEMM input.
 //
@@ -155,7 +160,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
             if (s < r) vA = sBeta[r] * accA[e] * dec;
           }
           sA[r * L::LDA + s] = vA;
-          Pout[r * kChunk + s] = E::from_f32(vP);
+          Pout[r * kChunk + (s & ~31) + kmap_pos(s & 31)] = E::from_f32(vP);
         }
       }
     } else {
@@ -166,7 +171,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         float xk[8], xq[8];
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const int d = kb * 32 + kmap(grp, j);
+          const int d = kb * 32 + kc(grp, j);
           const float ex = __expf(sGam[ra * L::LDG + d] - sGam[rho * L::LDG + d]);
           xk[j] = E::to_f32(sK[ra * L::LDK + d]) * ex;
           xq[j] = ra < len ? E::to_f32(qrow[d]) * ex : 0.f;
@@ -182,7 +187,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
           float xb[8];
 #pragma unroll
           for (int jj = 0; jj < 8; ++jj) {
-            const int d = kb * 32 + kmap(grp, jj);
+            const int d = kb * 32 + kc(grp, jj);
             xb[jj] = E::to_f32(sK[sb * L::LDK + d]) *
                      __expf(sGam[rho * L::LDG + d] - sGam[sb * L::LDG + d]);
           }
@@ -194,7 +199,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         for (int e = 0; e < 4; ++e) {
           const int r = r0 + 4 * grp + e;
           sA[r * L::LDA + sb] = sBeta[r] * accA[e];
-          Pout[r * kChunk + sb] = E::from_f32(accP[e]);
+          Pout[r * kChunk + (sb & ~31) + kmap_pos(sb & 31)] = E::from_f32(accP[e]);
         }
       }
       {  // diagonal block: elementwise fp32
@@ -217,7 +222,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         for (int e = 0; e < 4; ++e) {
           const int r = r0 + 4 * grp + e;
           sA[r * L::LDA + s] = s < r ? sBeta[r] * accA[e] : 0.f;
-          Pout[r * kChunk + s] = E::from_f32(s <= r ? accP[e] : 0.f);
+          Pout[r * kChunk + (s & ~31) + kmap_pos(s & 31)] = E::from_f32(s <= r ? accP[e] : 0.f);
         }
       }
       for (int j = i + 1; j < 4; ++j) {  // above the diagonal: zero
@@ -226,7 +231,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         for (int e = 0; e < 4; ++e) {
           const int r = r0 + 4 * grp + e;
           sA[r * L::LDA + s] = 0.f;
-          Pout[r * kChunk + s] = E::from_f32(0.f);
+          Pout[r * kChunk + (s & ~31) + kmap_pos(s & 31)] = E::from_f32(0.f);
         }
       }
     }
@@ -260,30 +265,47 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
     const int t2 = tid - 64;
     T *kt_out = static_cast<T *>(a.Kt) + blk * ((size_t)DK * kChunk);
     for (int idx = t2; idx < DK * kChunk / V; idx += kLocalThreads - 64) {
-      const int d = idx / (kChunk / V), s0 = (idx % (kChunk / V)) * V;
-      const uint4 u = *reinterpret_cast<const uint4 *>(sKt + d * L::LDT + s0);
+      // output positions p0..p0+V-1 of row d; position p holds logical token
+      // (p & ~31) + kmap((p & 31) >> 3, p & 7) -- the kmap-permuted layout the
+      // state kernel pairs with its accumulator-derived U fragments
+      const int d = idx / (kChunk / V), p0 = (idx % (kChunk / V)) * V;
       float outv[V];
 #pragma unroll
       for (int j = 0; j < V; ++j) {
-        const int s = s0 + j;
+        const int p = p0 + j;
+        const int s = (p & ~31) + kmap((p & 31) >> 3, p & 7);
         const float ex = KDA ? __expf(sGam[(kChunk - 1) * L::LDG + d] - sGam[s * L::LDG + d])
                              : __expf(sGam[kChunk - 1] - sGam[s]);
-        outv[j] = Vec16<T>::get(u, j) * ex;
+        outv[j] = E::to_f32(sKt[d * L::LDT + s]) * ex;
       }
-      *reinterpret_cast<uint4 *>(kt_out + (size_t)d * kChunk + s0) = Vec16<T>::pack(outv);
+      *reinterpret_cast<uint4 *>(kt_out + (size_t)d * kChunk + p0) = Vec16<T>::pack(outv);
     }
+    // Qt = Q * e^gamma, kmap-permuted along d_k: item (r, kb, g) writes the 8
+    // elements at positions kb*32 + 8g + j, i.e. logical d = kb*32 + kmap(g, j),
+    // read as two runs of 4 from q
     T *qt_out = static_cast<T *>(a.Qt) + blk * ((size_t)kChunk * DK);
-    for (int idx = t2; idx < kChunk * DK / V; idx += kLocalThreads - 64) {
-      const int r = idx / (DK / V), cv = (idx % (DK / V)) * V;
-      uint4 u = make_uint4(0, 0, 0, 0);
-      if (r < len) u = *reinterpret_cast<const uint4 *>(qbase + (size_t)r * qk_row + cv);
-      float outv[V];
-#pragma unroll
-      for (int j = 0; j < V; ++j) {
-        const float ex = KDA ? __expf(sGam[r * L::LDG + cv + j]) : __expf(sGam[r]);
-        outv[j] = Vec16<T>::get(u, j) * ex;
+    for (int idx = t2; idx < kChunk * DK / 8; idx += kLocalThreads - 64) {
+      const int r = idx / (DK / 8), kb = (idx % (DK / 8)) >> 2, g = idx & 3;
+      const int d0 = kb * 32 + 4 * g, d1 = kb * 32 + 16 + 4 * g;
+      f32x4 x0 = zero4(), x1 = zero4();
+      if (r < len) {
+        x0 = load4(qbase + (size_t)r * qk_row + d0);
+        x1 = load4(qbase + (size_t)r * qk_row + d1);
       }
-      *reinterpret_cast<uint4 *>(qt_out + (size_t)r * DK + cv) = Vec16<T>::pack(outv);
+      float outv[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        outv[j] = x0[j] * (KDA ? __expf(sGam[r * L::LDG + d0 + j]) : __expf(sGam[r]));
+        outv[4 + j] = x1[j] * (KDA ? __expf(sGam[r * L::LDG + d1 + j]) : __expf(sGam[r]));
+      }
+      T *dst = qt_out + (size_t)r * DK + kb * 32 + 8 * g;
+      if constexpr (sizeof(T) == 2) {
+        *reinterpret_cast<uint4 *>(dst) = Vec16<T>::pack(outv);
+      } else {
+        const float a0[4] = {outv[0], outv[1], outv[2], outv[3]}, a1[4] = {outv[4], outv[5], outv[6], outv[7]};
+        *reinterpret_cast<uint4 *>(dst) = Vec16<T>::pack(a0);
+        *reinterpret_cast<uint4 *>(dst + 4) = Vec16<T>::pack(a1);
+      }
     }
     float *dec_out = a.dec + blk * DK;
     if constexpr (KDA) {
@@ -305,7 +327,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       float xu[8], xw[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const int s = kb * 32 + kmap(grp, j);
+        const int s = kb * 32 + kc(grp, j);
         const float t = trow[j] * sBeta[s];
         xu[j] = t;
         xw[j] = KDA ? t : t * __expf(sGam[s]);
@@ -338,14 +360,17 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
           float xk[8];
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
-            const int s = kb * 32 + kmap(grp, j);
+            const int s = kb * 32 + kc(grp, j);
             xk[j] = E::to_f32(sKt[d * L::LDT + s]) * __expf(sGam[s * L::LDG + d]);
           }
           kf = make_frag<T>(xk);
         }
         acc = mma(acc, kf, tw[kb]);
       }
-      store4(w_out + (size_t)(16 * i + col) * DK + 16 * m + 4 * grp, acc);
+      // rows d = 16m + 4grp + e of this lane, stored negated and kmap-permuted
+      // inside their 32-block (logical index (m & 1) * 16 + 4grp + e sits at
+      // 8grp + 4(m & 1) + e)
+      store4(w_out + (size_t)(16 * i + col) * DK + (m >> 1) * 32 + 8 * grp + 4 * (m & 1), -acc);
     }
   }
 }

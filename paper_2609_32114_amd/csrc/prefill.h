@@ -13,7 +13,7 @@ constexpr int kChunk = 64;  // chunk length C (paper Sec. 7.1 uses C = 64)
 // Everything one prefill call needs, resolved to device pointers.  The
 // workspace regions are carved by api.cpp; per (chunk, value head) block
 // `blk = chunk * Hv + h` each region holds one fixed-size block:
-//   W   [64][Dk]    W = T Diag(b) (K * e^gamma)       (op #4; Sec. 5 "W = A^-1 K")
+//   W   [64][Dk]    -W, W = T Diag(b) (K * e^gamma)   (op #4; Sec. 5 "W = A^-1 K")
 //   Ut  [Dv][64]    U~^T, U~ = T Diag(b) V            (op #4)
 //   Kt  [Dk][64]    (K * e^(gamma_last - gamma))^T    (keys as op #5-update uses them)
 //   Qt  [64][Dk]    Q * e^gamma                       (queries as op #6 uses them)
@@ -21,7 +21,11 @@ constexpr int kChunk = 64;  // chunk length C (paper Sec. 7.1 uses C = 64)
 //   dec [Dk]        e^gamma_last (GDN: element 0 only)
 //   U   [Dv][64]    U^T, U = U~ - W S_c^T  (the "v_c" of op #5-read, Sec. 5)
 //   Hs  [Dv][Dk]    S_c, the state entering the chunk (snapshot for op #6)
-// Element type of W/Ut/Kt/Qt/P/U/Hs is the I/O dtype (bf16 or fp32).
+// Element type of every block is the I/O dtype (bf16 or fp32).  Inside each
+// 32-block along the contracted index, W (d_k), Kt (tokens), Qt (d_k), P
+// (tokens), U (tokens) and Hs (d_k) are kmap-permuted (device.h): W and Kt
+// pair with accumulator-derived fragments in the state kernel, U and Hs are
+// written as those fragments, Qt and P pair with them in the output kernel.
 struct PrefillArgs {
   const void *q, *k, *v;
   const float *g, *beta, *s0;
