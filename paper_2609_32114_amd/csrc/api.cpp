@@ -43,7 +43,7 @@ bool add_ok(size_t a, size_t b, size_t *out) { return !__builtin_add_overflow(a,
 
 // Byte offsets of every workspace region (each 256-byte aligned).
 struct Layout {
-  size_t status, seq_info, chunk_info, W, Ut, Kt, Qt, P, dec, U, Hs, total;
+  size_t status, seq_info, chunk_info, NM, Bc, Qp, Ol, P, dec, Hs, total;
   int max_chunks;
 };
 
@@ -73,13 +73,12 @@ bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, Layout *L) {
   L->status = region(1, sizeof(int), 1);
   L->seq_info = region(1, sizeof(int4), (size_t)N);
   L->chunk_info = region(1, sizeof(int4), mc);
-  L->W = region(C * Dk, esz, blocks);
-  L->Ut = region((size_t)Dv * C, esz, blocks);
-  L->Kt = region((size_t)Dk * C, esz, blocks);
-  L->Qt = region(C * Dk, esz, blocks);
+  L->NM = region((size_t)Dk * Dk, esz, blocks);
+  L->Bc = region((size_t)Dv * Dk, esz, blocks);
+  L->Qp = region(C * Dk, esz, blocks);
+  L->Ol = region(C * Dv, esz, blocks);
   L->P = region(C * C, esz, blocks);
   L->dec = region((size_t)Dk, sizeof(float), blocks);
-  L->U = region((size_t)Dv * C, esz, blocks);
   L->Hs = region((size_t)Dv * Dk, esz, blocks);
   L->total = (off + kAlign - 1) / kAlign * kAlign;
   if (!ok) fail(HAGDN_EINVAL, "workspace size overflows");
@@ -162,9 +161,9 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   a.status = reinterpret_cast<int *>(w + L.status);
   a.seq_info = reinterpret_cast<int4 *>(w + L.seq_info);
   a.chunk_info = reinterpret_cast<int4 *>(w + L.chunk_info);
-  a.W = w + L.W; a.Ut = w + L.Ut; a.Kt = w + L.Kt; a.Qt = w + L.Qt; a.P = w + L.P;
+  a.NM = w + L.NM; a.Bc = w + L.Bc; a.Qp = w + L.Qp; a.Ol = w + L.Ol; a.P = w + L.P;
   a.dec = reinterpret_cast<float *>(w + L.dec);
-  a.U = w + L.U; a.Hs = w + L.Hs;
+  a.Hs = w + L.Hs;
 
   hipStream_t st = static_cast<hipStream_t>(stream_);
   hipEvent_t *ev = nullptr;

@@ -177,6 +177,26 @@ template <> __device__ __forceinline__ f32x8 frag_from_acc<float>(f32x4 lo, f32x
   return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
+// Fragment-order ("swizzled") blocks: a 16x32 operand block stored as 64 lanes
+// x 8 consecutive elements, lane-major, exactly as the MFMA fragment sits in a
+// wave.  A wave reads or writes one such block as a single contiguous 1 KiB
+// (bf16) run.  load_frag_at / store_frag_at address this lane's 8 elements.
+__device__ __forceinline__ bf16x8 load_frag_at(const bf16_t *p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(p));
+}
+__device__ __forceinline__ f32x8 load_frag_at(const float *p) {
+  const f32x4 a = *reinterpret_cast<const f32x4 *>(p);
+  const f32x4 b = *reinterpret_cast<const f32x4 *>(p + 4);
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+__device__ __forceinline__ void store_frag_at(bf16_t *p, bf16x8 f) {
+  *reinterpret_cast<uint4 *>(p) = __builtin_bit_cast(uint4, f);
+}
+__device__ __forceinline__ void store_frag_at(float *p, f32x8 f) {
+  *reinterpret_cast<f32x4 *>(p) = __builtin_shufflevector(f, f, 0, 1, 2, 3);
+  *reinterpret_cast<f32x4 *>(p + 4) = __builtin_shufflevector(f, f, 4, 5, 6, 7);
+}
+
 // Store a fragment where load_frag would read it: 8 elements at p + 8*grp.
 __device__ __forceinline__ void store_frag(bf16_t *p, bf16x8 f, int grp) {
   *reinterpret_cast<uint4 *>(p + 8 * grp) = __builtin_bit_cast(uint4, f);

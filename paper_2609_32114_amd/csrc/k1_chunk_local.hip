@@ -1,6 +1,8 @@
 // k1_chunk_local.hip -- the first Map phase of chunkwise delta-rule prefill
 // (paper Sec. 2.1: operators #1 Gate, #2 KKT, #3 Solve, #4 W/U), one
-// workgroup per (chunk, value head), fully parallel over both.
+// workgroup per (chunk, value head), fully parallel over both, plus the
+// chunk-local products that let the sequential kernel advance the state with
+// a single product per chunk.
 //
 // For a chunk of n <= 64 tokens (rows >= n are zero-padded, which makes them
 // contribute nothing downstream), with gamma the inclusive cumulative
@@ -10,15 +12,18 @@
 //       P[r][s] =     <q_r, e^(gamma_r - gamma_s) k_s>           (s <= r)
 //   #3  T = (I + A)^-1                       (unit lower triangular, fp32)
 //   #4  W  = T Diag(b) (K * e^gamma)         U~ = T Diag(b) V
-// plus the operands the sequential kernel and the output kernel consume:
-//   Kt = (K * e^(gamma_last - gamma))^T,  Qt = Q * e^gamma,  dec = e^gamma_last.
-// W and Kt are the A operands of the state kernel's chained products and are
-// stored kmap-permuted inside each 32-block (see device.h), W negated; Qt and P
-// are the partners of the state kernel's fragment-order outputs (snapshot,
-// corrected values) in the output kernel and are kmap-permuted along d_k and
-// along tokens respectively.  Ut is stored in logical order.
-// P is the decay-masked Q K^T of Sec. 5's GEMM group (KK^T and QK^T share K
-// and are computed together); the solve never has to wait on a GEMM input.
+// With Kt = (K * e^(gamma_last - gamma))^T and D = Diag(e^gamma_last), the
+// state update of operator #5 and the output of operator #6 are affine in the
+// state S_c entering the chunk (S^T, d_k x d_v):
+//   S^T_{c+1} = D S^T_c - M S^T_c + B,        M = Kt W,  B = Kt U~
+//   O         = Q' S^T_c + O_loc,             Q' = Q * e^gamma - P W,  O_loc = P U~
+// (expand U = U~ - W S^T_c, the corrected values "v_c" of Sec. 5, in
+// S^T_{c+1} = D S^T_c + Kt U and O = (Q * e^gamma) S^T_c + P U).  This
+// kernel computes the state-independent factors -M, B, Q', O_loc and the
+// chunk decay; W and U~ never leave the workgroup.  It is Sec. 5's GEMM-first
+// regrouping carried one step further: every product that does not need the
+// incoming state runs here, chunk-parallel, so the sequential kernel's
+// critical path per chunk is one product.
 //
 // GDN's decay is a scalar per token, so K K^T and Q K^T are plain MFMA
 // products and the decay is applied in the epilogue.  KDA's per-channel decay
@@ -29,7 +34,8 @@
 //
 // Wave roles (4 waves): wave i computes row block i of A and P; wave 0 then
 // solves T by forward substitution (lane j owns column j) while waves 1-3
-// write Kt, Qt and dec; finally wave i computes token block i of W and U~.
+// write the decay; wave i computes token block i of W and U~ into LDS; then
+// the four reduce-side products are split over the waves.
 #include "device.h"
 #include "prefill.h"
 
@@ -40,17 +46,21 @@ constexpr int kLocalThreads = 256;
 template <typename T, int DK, int DV, bool KDA>
 struct LocalLayout {
   static constexpr int PAD = 16 / (int)sizeof(T);
-  static constexpr int LDK = DK + PAD;       // sK   [64][LDK]   keys, token rows
+  static constexpr int LDK = DK + PAD;       // sK   [64][LDK]   keys, token rows (ops #2)
   static constexpr int LDT = kChunk + PAD;   // sKt  [DK][LDT]   keys, channel rows
-                                             // sVt  [DV][LDT]   values, channel rows
+                                             // sVt  [DV][LDT]   values, channel rows (op #4)
+                                             // sWt  [DK][LDT]   W, channel rows (over sK)
+                                             // sUt  [DV][LDT]   U~, channel rows (over sVt)
   static constexpr int LDA = kChunk + 4;     // sA   [64][LDA]   A, then T (fp32)
   static constexpr int LDG = KDA ? DK + 1 : 1;  // sGam [64][LDG] (GDN: [64])
-  static constexpr size_t off_K = 0;
-  static constexpr size_t off_Kt = off_K + sizeof(T) * kChunk * LDK;
-  static constexpr size_t off_Vt = off_Kt + sizeof(T) * DK * LDT;
+  static constexpr size_t bytesX = sizeof(T) * (kChunk * LDK > DK * LDT ? kChunk * LDK : DK * LDT);
+  static constexpr size_t off_K = 0;         // region X: sK, later sWt
+  static constexpr size_t off_Kt = off_K + bytesX;
+  static constexpr size_t off_Vt = off_Kt + sizeof(T) * DK * LDT;   // region Y: sVt, later sUt
   static constexpr size_t off_A = off_Vt + sizeof(T) * DV * LDT;
   static constexpr size_t off_beta = off_A + sizeof(float) * kChunk * LDA;
-  static constexpr size_t off_gam = off_beta + sizeof(float) * kChunk;
+  static constexpr size_t off_kdec = off_beta + sizeof(float) * kChunk;  // GDN e^(gamma_last - gamma_s)
+  static constexpr size_t off_gam = off_kdec + sizeof(float) * kChunk;
   static constexpr size_t bytes = off_gam + sizeof(float) * kChunk * LDG;
 };
 
@@ -75,7 +85,10 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
   T *sVt = reinterpret_cast<T *>(smem + L::off_Vt);
   float *sA = reinterpret_cast<float *>(smem + L::off_A);
   float *sBeta = reinterpret_cast<float *>(smem + L::off_beta);
+  float *sKdec = reinterpret_cast<float *>(smem + L::off_kdec);
   float *sGam = reinterpret_cast<float *>(smem + L::off_gam);
+  T *sWt = sK;   // reuses region X once op #2 is done with the keys
+  T *sUt = sVt;  // reuses region Y once op #4 has read the values
 
   const size_t qk_row = (size_t)a.Hqk * DK;  // token stride of q and k
   const size_t v_row = (size_t)a.Hv * DV;
@@ -160,7 +173,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
             if (s < r) vA = sBeta[r] * accA[e] * dec;
           }
           sA[r * L::LDA + s] = vA;
-          Pout[r * kChunk + (s & ~31) + kmap_pos(s & 31)] = E::from_f32(vP);
+          Pout[r * kChunk + s] = E::from_f32(vP);
         }
       }
     } else {
@@ -199,7 +212,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         for (int e = 0; e < 4; ++e) {
           const int r = r0 + 4 * grp + e;
           sA[r * L::LDA + sb] = sBeta[r] * accA[e];
-          Pout[r * kChunk + (sb & ~31) + kmap_pos(sb & 31)] = E::from_f32(accP[e]);
+          Pout[r * kChunk + sb] = E::from_f32(accP[e]);
         }
       }
       {  // diagonal block: elementwise fp32
@@ -222,7 +235,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         for (int e = 0; e < 4; ++e) {
           const int r = r0 + 4 * grp + e;
           sA[r * L::LDA + s] = s < r ? sBeta[r] * accA[e] : 0.f;
-          Pout[r * kChunk + (s & ~31) + kmap_pos(s & 31)] = E::from_f32(s <= r ? accP[e] : 0.f);
+          Pout[r * kChunk + s] = E::from_f32(s <= r ? accP[e] : 0.f);
         }
       }
       for (int j = i + 1; j < 4; ++j) {  // above the diagonal: zero
@@ -231,7 +244,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         for (int e = 0; e < 4; ++e) {
           const int r = r0 + 4 * grp + e;
           sA[r * L::LDA + s] = 0.f;
-          Pout[r * kChunk + (s & ~31) + kmap_pos(s & 31)] = E::from_f32(0.f);
+          Pout[r * kChunk + s] = E::from_f32(0.f);
         }
       }
     }
@@ -261,63 +274,22 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 #pragma unroll
     for (int r = 0; r < kChunk; ++r) sA[r * L::LDA + lane] = x[r];
   } else {
-    // ---- operands for the sequential and output kernels (threads 64..255)
+    // chunk decay e^gamma_last, and (GDN) each token's key decay to the chunk end
     const int t2 = tid - 64;
-    T *kt_out = static_cast<T *>(a.Kt) + blk * ((size_t)DK * kChunk);
-    for (int idx = t2; idx < DK * kChunk / V; idx += kLocalThreads - 64) {
-      // output positions p0..p0+V-1 of row d; position p holds logical token
-      // (p & ~31) + kmap((p & 31) >> 3, p & 7) -- the kmap-permuted layout the
-      // state kernel pairs with its accumulator-derived U fragments
-      const int d = idx / (kChunk / V), p0 = (idx % (kChunk / V)) * V;
-      float outv[V];
-#pragma unroll
-      for (int j = 0; j < V; ++j) {
-        const int p = p0 + j;
-        const int s = (p & ~31) + kmap((p & 31) >> 3, p & 7);
-        const float ex = KDA ? __expf(sGam[(kChunk - 1) * L::LDG + d] - sGam[s * L::LDG + d])
-                             : __expf(sGam[kChunk - 1] - sGam[s]);
-        outv[j] = E::to_f32(sKt[d * L::LDT + s]) * ex;
-      }
-      *reinterpret_cast<uint4 *>(kt_out + (size_t)d * kChunk + p0) = Vec16<T>::pack(outv);
-    }
-    // Qt = Q * e^gamma, kmap-permuted along d_k: item (r, kb, g) writes the 8
-    // elements at positions kb*32 + 8g + j, i.e. logical d = kb*32 + kmap(g, j),
-    // read as two runs of 4 from q
-    T *qt_out = static_cast<T *>(a.Qt) + blk * ((size_t)kChunk * DK);
-    for (int idx = t2; idx < kChunk * DK / 8; idx += kLocalThreads - 64) {
-      const int r = idx / (DK / 8), kb = (idx % (DK / 8)) >> 2, g = idx & 3;
-      const int d0 = kb * 32 + 4 * g, d1 = kb * 32 + 16 + 4 * g;
-      f32x4 x0 = zero4(), x1 = zero4();
-      if (r < len) {
-        x0 = load4(qbase + (size_t)r * qk_row + d0);
-        x1 = load4(qbase + (size_t)r * qk_row + d1);
-      }
-      float outv[8];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        outv[j] = x0[j] * (KDA ? __expf(sGam[r * L::LDG + d0 + j]) : __expf(sGam[r]));
-        outv[4 + j] = x1[j] * (KDA ? __expf(sGam[r * L::LDG + d1 + j]) : __expf(sGam[r]));
-      }
-      T *dst = qt_out + (size_t)r * DK + kb * 32 + 8 * g;
-      if constexpr (sizeof(T) == 2) {
-        *reinterpret_cast<uint4 *>(dst) = Vec16<T>::pack(outv);
-      } else {
-        const float a0[4] = {outv[0], outv[1], outv[2], outv[3]}, a1[4] = {outv[4], outv[5], outv[6], outv[7]};
-        *reinterpret_cast<uint4 *>(dst) = Vec16<T>::pack(a0);
-        *reinterpret_cast<uint4 *>(dst + 4) = Vec16<T>::pack(a1);
-      }
-    }
     float *dec_out = a.dec + blk * DK;
     if constexpr (KDA) {
       for (int d = t2; d < DK; d += kLocalThreads - 64)
         dec_out[d] = __expf(sGam[(kChunk - 1) * L::LDG + d]);
     } else {
+      if (t2 < kChunk) sKdec[t2] = __expf(sGam[kChunk - 1] - sGam[t2]);
       if (t2 == 0) dec_out[0] = __expf(sGam[kChunk - 1]);
     }
   }
   __syncthreads();
 
-  // ---- op #4: wave i = token block i.  T' = T Diag(b) (GDN: also e^gamma_s)
+  // ---- op #4: wave i = token block i.  T' = T Diag(b) (GDN: also e^gamma_s).
+  // W and U~ go to LDS as channel rows: sWt[d_k][token] (region X, free since
+  // op #2), sUt[d_v][token] (region Y, once every wave has read the values).
   {
     const int i = wave, r = 16 * i + col;
     Frag<T> tu[2], tw[2];
@@ -335,21 +307,18 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       tu[kb] = make_frag<T>(xu);
       tw[kb] = make_frag<T>(xw);
     }
-    // U~ = T Diag(b) V: rows = tokens, columns = d_v; stored transposed [d_v][token]
-    T *ut_out = static_cast<T *>(a.Ut) + blk * ((size_t)DV * kChunk);
+    // U~ rows = tokens, columns = d_v; W rows = tokens, columns = d_k
+    f32x4 accU[DV / 16];
 #pragma unroll
     for (int n = 0; n < DV / 16; ++n) {
-      f32x4 acc = zero4();
+      accU[n] = zero4();
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-        acc = mma(acc, tu[kb], load_frag(sVt + (16 * n + col) * L::LDT + kb * 32, grp));
-      store4(ut_out + (size_t)(16 * n + col) * kChunk + 16 * i + 4 * grp, acc);
+        accU[n] = mma(accU[n], tu[kb], load_frag(sVt + (16 * n + col) * L::LDT + kb * 32, grp));
     }
-    // W^T = (K e^gamma)^T T'^T: rows = d_k, columns = tokens; stored [token][d_k]
-    T *w_out = static_cast<T *>(a.W) + blk * ((size_t)kChunk * DK);
 #pragma unroll
-    for (int m = 0; m < DK / 16; ++m) {
-      const int d = 16 * m + col;
+    for (int n = 0; n < DK / 16; ++n) {
+      const int d = 16 * n + col;
       f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
@@ -365,12 +334,101 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
           }
           kf = make_frag<T>(xk);
         }
-        acc = mma(acc, kf, tw[kb]);
+        acc = mma(acc, tw[kb], kf);
       }
-      // rows d = 16m + 4grp + e of this lane, stored negated and kmap-permuted
-      // inside their 32-block (logical index (m & 1) * 16 + 4grp + e sits at
-      // 8grp + 4(m & 1) + e)
-      store4(w_out + (size_t)(16 * i + col) * DK + (m >> 1) * 32 + 8 * grp + 4 * (m & 1), -acc);
+      // lane: column d, rows (tokens) 16i + 4grp + e
+      store4(sWt + d * L::LDT + 16 * i + 4 * grp, acc);
+    }
+    __syncthreads();  // every wave has read sVt
+#pragma unroll
+    for (int n = 0; n < DV / 16; ++n) store4(sUt + (16 * n + col) * L::LDT + 16 * i + 4 * grp, accU[n]);
+  }
+  __syncthreads();
+
+  // ---- reduce-side products.  Kt fragments are built from the staged keys:
+  //      Kt[d][s] = K[s][d] e^(gamma_last - gamma_s)  (KDA: per channel d)
+  constexpr int KT = DK / 16, VT = DV / 16;
+  constexpr int KPW = KT / 4;  // d_k tiles per wave
+  auto kt_frag = [&](int d, int kb) {
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int s = kb * 32 + kc(grp, j);
+      const float ex = KDA ? __expf(sGam[(kChunk - 1) * L::LDG + d] - sGam[s * L::LDG + d]) : sKdec[s];
+      x[j] = E::to_f32(sKt[d * L::LDT + s]) * ex;
+    }
+    return make_frag<T>(x);
+  };
+  {
+    // (a) -M = -(Kt W), the state kernel's A operand (fragment order, prefill.h).
+    //     Computed transposed, M^T = W^T Kt^T: rows d_in from sWt, columns
+    //     d_out from Kt.
+    T *nm_out = static_cast<T *>(a.NM) + blk * ((size_t)DK * DK);
+#pragma unroll
+    for (int nn = 0; nn < KPW; ++nn) {
+      const int n = wave * KPW + nn, dout = 16 * n + col;  // this lane's B column
+      const Frag<T> bk[2] = {kt_frag(dout, 0), kt_frag(dout, 1)};
+#pragma unroll
+      for (int m = 0; m < KT; ++m) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+          acc = mma(acc, load_frag(sWt + (16 * m + col) * L::LDT + kb * 32, grp), bk[kb]);
+        // lane: column d_out, rows d_in = 16m + 4grp + e = 32(m >> 1) + kmap(grp, 4(m & 1) + e)
+        // -> slots 4(m & 1) + e of operand block (t = n, kb = m >> 1)
+        store4(nm_out + ((size_t)(n * (DK / 32) + (m >> 1)) * 64 + lane) * 8 + 4 * (m & 1), -acc);
+      }
+    }
+    // (b) B = Kt U~, the state kernel's accumulator init (fragment order)
+    T *b_out = static_cast<T *>(a.Bc) + blk * ((size_t)DV * DK);
+#pragma unroll
+    for (int mm = 0; mm < KPW; ++mm) {
+      const int m = wave * KPW + mm;
+      const Frag<T> ak[2] = {kt_frag(16 * m + col, 0), kt_frag(16 * m + col, 1)};
+#pragma unroll
+      for (int n = 0; n < VT; ++n) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+          acc = mma(acc, ak[kb], load_frag(sUt + (16 * n + col) * L::LDT + kb * 32, grp));
+        store4(b_out + ((size_t)(n * (DK / 16) + m) * 64 + lane) * 4, acc);
+      }
+    }
+    // (c) Q' = Q e^gamma - P W and (d) O_loc = P U~, the output kernel's B
+    //     operand and accumulator init (fragment order, token tile nt = w);
+    //     computed transposed (rows = channels, columns = tokens 16w..16w+15).
+    //     P is causal: k-blocks kb <= w/2.
+    const int r = 16 * wave + col;
+    const T *prow = static_cast<const T *>(a.P) + blk * (kChunk * kChunk) + (size_t)r * kChunk;
+    Frag<T> bp[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) bp[kb] = load_frag(prow + kb * 32, grp);
+    const int nkb = (wave >> 1) + 1;
+    T *qp_out = static_cast<T *>(a.Qp) + blk * ((size_t)kChunk * DK) + (size_t)wave * (DK / 32) * 64 * 8;
+    const T *qrow = qbase + (size_t)r * qk_row;
+#pragma unroll
+    for (int m = 0; m < KT; ++m) {
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        if (kb < nkb) acc = mma(acc, load_frag(sWt + (16 * m + col) * L::LDT + kb * 32, grp), bp[kb]);
+      const int d = 16 * m + 4 * grp;
+      f32x4 qe = zero4();
+      if (r < len) {
+        qe = load4(qrow + d);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) qe[e] *= KDA ? __expf(sGam[r * L::LDG + d + e]) : __expf(sGam[r]);
+      }
+      store4(qp_out + ((size_t)(m >> 1) * 64 + lane) * 8 + 4 * (m & 1), qe - acc);
+    }
+    T *ol_out = static_cast<T *>(a.Ol) + blk * ((size_t)kChunk * DV) + (size_t)wave * (DV / 16) * 64 * 4;
+#pragma unroll
+    for (int m = 0; m < VT; ++m) {
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        if (kb < nkb) acc = mma(acc, load_frag(sUt + (16 * m + col) * L::LDT + kb * 32, grp), bp[kb]);
+      store4(ol_out + ((size_t)m * 64 + lane) * 4, acc);
     }
   }
 }

@@ -1,15 +1,17 @@
 // k3_output.hip -- the final Map phase of chunkwise delta-rule prefill
 // (paper Sec. 2.1, operator #6 O), one workgroup per (chunk, value head),
-// fully parallel.  Operator #6 needs only the state entering the chunk and the
-// corrected values v_c (paper Sec. 5, "Cross-Chunk"):
+// fully parallel.  Operator #6 needs only the state S_c entering the chunk
+// and chunk-local factors (paper Sec. 5, "Cross-Chunk"); with the factors of
+// the chunk-local kernel it is one product:
 //
-//   O = scale * ( (Q * e^gamma) S_c^T + P U )      P = decay-masked Q K^T, s <= r
+//   O = scale * (Q' S^T_c + O_loc),   Q' = Q * e^gamma - P W,  O_loc = P U~
 //
-// computed transposed, O^T = S_c (Q e^gamma)^T + U^T P^T, so that each lane's
+// computed transposed, O^T = S_c Q'^T + O_loc^T, so that each lane's
 // accumulator holds 4 consecutive d_v values of one token (an 8-byte bf16
-// store into o[token][head][d_v]).  Wave w owns d_v rows [w*DV/4, (w+1)*DV/4)
-// for all 64 tokens, so each wave reads its slice of the snapshot once.  The
-// causal structure of P skips k-blocks of U above the diagonal.
+// store into o[token][head][d_v]).  The snapshot S_c, Q' and O_loc arrive in
+// fragment order (prefill.h): every operand load is one contiguous 1 KiB run
+// per wave, and the S_c and Q' fragments pair directly.  Wave w owns d_v rows
+// [w*DV/4, (w+1)*DV/4) for all 64 tokens.
 #include "device.h"
 #include "prefill.h"
 
@@ -29,31 +31,23 @@ __global__ __launch_bounds__(kOutThreads) void output_kernel(PrefillArgs a) {
   const int col = lane & 15, grp = lane >> 4;
   const size_t blk = (size_t)c * a.Hv + h;
   const T *hs = static_cast<const T *>(a.Hs) + blk * ((size_t)DV * DK);
-  const T *qt = static_cast<const T *>(a.Qt) + blk * ((size_t)kChunk * DK);
-  const T *u = static_cast<const T *>(a.U) + blk * ((size_t)DV * kChunk);
-  const T *p = static_cast<const T *>(a.P) + blk * ((size_t)kChunk * kChunk);
+  const T *qp = static_cast<const T *>(a.Qp) + blk * ((size_t)kChunk * DK);
+  const T *ol = static_cast<const T *>(a.Ol) + blk * ((size_t)kChunk * DV);
   T *o = static_cast<T *>(a.o);
 
 #pragma unroll
   for (int mi = 0; mi < MPW; ++mi) {
     const int m = wave * MPW + mi;      // d_v tile
-    const int dv_row = 16 * m + col;    // A-operand row this lane feeds
-    Frag<T> sa[DK / 32];
+    Frag<T> sa[DK / 32];  // snapshot blocks (d_v tile m, kb), fragment order
 #pragma unroll
-    for (int kb = 0; kb < DK / 32; ++kb) sa[kb] = load_frag(hs + (size_t)dv_row * DK + kb * 32, grp);
-    Frag<T> ua[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) ua[kb] = load_frag(u + (size_t)dv_row * kChunk + kb * 32, grp);
+    for (int kb = 0; kb < DK / 32; ++kb) sa[kb] = load_frag_at(hs + ((size_t)(m * (DK / 32) + kb) * 64 + lane) * 8);
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {    // token tile
-      const int r = 16 * nt + col;      // B-operand column (token) this lane feeds
-      f32x4 acc = zero4();
+      const int r = 16 * nt + col;      // token this lane's accumulator column holds
+      f32x4 acc = load4(ol + ((size_t)(nt * (DV / 16) + m) * 64 + lane) * 4);
 #pragma unroll
       for (int kb = 0; kb < DK / 32; ++kb)
-        acc = mma(acc, sa[kb], load_frag(qt + (size_t)r * DK + kb * 32, grp));
-#pragma unroll
-      for (int kb = 0; kb <= nt / 2; ++kb)
-        acc = mma(acc, ua[kb], load_frag(p + (size_t)r * kChunk + kb * 32, grp));
+        acc = mma(acc, sa[kb], load_frag_at(qp + ((size_t)(nt * (DK / 32) + kb) * 64 + lane) * 8));
       if (r < len) store4(o + ((size_t)(start + r) * a.Hv + h) * DV + 16 * m + 4 * grp, acc * a.scale);
     }
   }

@@ -12,20 +12,32 @@ constexpr int kChunk = 64;  // chunk length C (paper Sec. 7.1 uses C = 64)
 
 // Everything one prefill call needs, resolved to device pointers.  The
 // workspace regions are carved by api.cpp; per (chunk, value head) block
-// `blk = chunk * Hv + h` each region holds one fixed-size block:
-//   W   [64][Dk]    -W, W = T Diag(b) (K * e^gamma)   (op #4; Sec. 5 "W = A^-1 K")
-//   Ut  [Dv][64]    U~^T, U~ = T Diag(b) V            (op #4)
-//   Kt  [Dk][64]    (K * e^(gamma_last - gamma))^T    (keys as op #5-update uses them)
-//   Qt  [64][Dk]    Q * e^gamma                       (queries as op #6 uses them)
-//   P   [64][64]    P[r][s] = <q_r, e^(gamma_r-gamma_s) k_s>, s <= r, else 0
-//   dec [Dk]        e^gamma_last (GDN: element 0 only)
-//   U   [Dv][64]    U^T, U = U~ - W S_c^T  (the "v_c" of op #5-read, Sec. 5)
-//   Hs  [Dv][Dk]    S_c, the state entering the chunk (snapshot for op #6)
-// Element type of every block is the I/O dtype (bf16 or fp32).  Inside each
-// 32-block along the contracted index, W (d_k), Kt (tokens), Qt (d_k), P
-// (tokens), U (tokens) and Hs (d_k) are kmap-permuted (device.h): W and Kt
-// pair with accumulator-derived fragments in the state kernel, U and Hs are
-// written as those fragments, Qt and P pair with them in the output kernel.
+// `blk = chunk * Hv + h` each region holds one fixed-size block.  With
+// Kt = (K * e^(gamma_last - gamma))^T, D = Diag(e^gamma_last) and W, U~, P
+// the chunk-local operators #2-#4 (see k1_chunk_local.hip):
+//   NM  -M = -(Kt W)                 (Dk x Dk: d_k out x d_k in)
+//   Bc  B = Kt U~                    (Dk x Dv)
+//   dec e^gamma_last                 (Dk floats; GDN: element 0 only)
+//   Qp  Q' = Q * e^gamma - P W       (64 x Dk)
+//   Ol  O_loc = P U~                 (64 x Dv)
+//   P   decay-masked Q K^T           (64 x 64, row-major; scratch of the first kernel)
+//   Hs  S_c, the state entering the chunk (as S^T, Dk x Dv)
+// so that  S^T_{c+1} = D S^T_c + NM S^T_c + B  and  O = scale (Q' S^T_c + O_loc).
+// NM, Bc, Qp, Ol and Hs are stored in fragment order (device.h): one 16-lane
+// by 32 (operands) or 16x16 (accumulators) block after another, 64 lanes x 8
+// (operand) or x 4 (accumulator) elements each, so every producer and consumer
+// moves whole blocks with contiguous 16- or 8-byte lane accesses:
+//   NM  operand blocks (row tile t of d_k out, k-block kb of d_k in), t-major;
+//       slot j of lane (col, grp) = NM[16t + col][32kb + kmap(grp, j)]
+//   Bc  accumulator blocks (d_v tile n, d_k tile m), n-major;
+//       element e of lane (col, grp) = B[16m + 4grp + e][16n + col]
+//   Hs  operand blocks (d_v tile n, k-block kb of d_k), n-major;
+//       slot j of lane (col, grp) = S^T[32kb + kmap(grp, j)][16n + col]
+//   Qp  operand blocks (token tile nt, k-block kb of d_k), nt-major;
+//       slot j of lane (col, grp) = Q'[16nt + col][32kb + kmap(grp, j)]
+//   Ol  accumulator blocks (token tile nt, d_v tile m), nt-major;
+//       element e of lane (col, grp) = O_loc[16nt + col][16m + 4grp + e]
+// Element type of every block is the I/O dtype (bf16 or fp32), dec is fp32.
 struct PrefillArgs {
   const void *q, *k, *v;
   const float *g, *beta, *s0;
@@ -39,7 +51,7 @@ struct PrefillArgs {
   int *status;         // [1] device status word (hagdn_device_code)
   int4 *seq_info;      // [N]  {first chunk, number of chunks, start token, length}
   int4 *chunk_info;    // [max_chunks] {sequence, start token, length, 0}; length 0 = unused
-  void *W, *Ut, *Kt, *Qt, *P, *U, *Hs;
+  void *NM, *Bc, *Qp, *Ol, *P, *Hs;
   float *dec;
 };
 
