@@ -43,7 +43,7 @@ bool add_ok(size_t a, size_t b, size_t *out) { return !__builtin_add_overflow(a,
 
 // Byte offsets of every workspace region (each 256-byte aligned).
 struct Layout {
-  size_t status, seq_info, chunk_info, NM, Bc, Qp, Ol, P, dec, Hs, total;
+  size_t status, seq_info, chunk_info, NM, Bc, Qp, Ol, dec, Hs, total;
   int max_chunks;
 };
 
@@ -77,7 +77,6 @@ bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, Layout *L) {
   L->Bc = region((size_t)Dv * Dk, esz, blocks);
   L->Qp = region(C * Dk, esz, blocks);
   L->Ol = region(C * Dv, esz, blocks);
-  L->P = region(C * C, esz, blocks);
   L->dec = region((size_t)Dk, sizeof(float), blocks);
   L->Hs = region((size_t)Dv * Dk, esz, blocks);
   L->total = (off + kAlign - 1) / kAlign * kAlign;
@@ -161,7 +160,7 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   a.status = reinterpret_cast<int *>(w + L.status);
   a.seq_info = reinterpret_cast<int4 *>(w + L.seq_info);
   a.chunk_info = reinterpret_cast<int4 *>(w + L.chunk_info);
-  a.NM = w + L.NM; a.Bc = w + L.Bc; a.Qp = w + L.Qp; a.Ol = w + L.Ol; a.P = w + L.P;
+  a.NM = w + L.NM; a.Bc = w + L.Bc; a.Qp = w + L.Qp; a.Ol = w + L.Ol;
   a.dec = reinterpret_cast<float *>(w + L.dec);
   a.Hs = w + L.Hs;
 

@@ -206,6 +206,10 @@ __device__ __forceinline__ void store_frag(float *p, f32x8 f, int grp) {
   *reinterpret_cast<f32x4 *>(p + 8 * grp + 4) = __builtin_shufflevector(f, f, 4, 5, 6, 7);
 }
 
+// Element j of a fragment as fp32 (exact).
+__device__ __forceinline__ float frag_elem(bf16x8 f, int j) { return (float)f[j]; }
+__device__ __forceinline__ float frag_elem(f32x8 f, int j) { return f[j]; }
+
 template <typename T> __device__ __forceinline__ Frag<T> zero_frag() {
   float x[8] = {0, 0, 0, 0, 0, 0, 0, 0};
   return make_frag<T>(x);

@@ -60,7 +60,8 @@ struct LocalLayout {
   static constexpr size_t off_A = off_Vt + sizeof(T) * DV * LDT;
   static constexpr size_t off_beta = off_A + sizeof(float) * kChunk * LDA;
   static constexpr size_t off_kdec = off_beta + sizeof(float) * kChunk;  // GDN e^(gamma_last - gamma_s)
-  static constexpr size_t off_gam = off_kdec + sizeof(float) * kChunk;
+  static constexpr size_t off_tot = off_kdec + sizeof(float) * kChunk;   // KDA gate-scan segment totals
+  static constexpr size_t off_gam = off_tot + sizeof(float) * (KDA ? kLocalThreads : 0);
   static constexpr size_t bytes = off_gam + sizeof(float) * kChunk * LDG;
 };
 
@@ -68,7 +69,10 @@ template <typename T, int DK, int DV, bool KDA>
 __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs a) {
   using L = LocalLayout<T, DK, DV, KDA>;
   using E = Elt<T>;
+  using V16 = Vec16<T>;
   constexpr int V = 16 / (int)sizeof(T);  // elements per 16-byte vector
+  constexpr int KT = DK / 16, VT = DV / 16;
+  constexpr int KPW = KT / 4;             // d_k tiles per wave in the reduce-side products
   const int c = blockIdx.x, h = blockIdx.y;
   const int4 ci = a.chunk_info[c];
   const int len = ci.z;
@@ -86,6 +90,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
   float *sA = reinterpret_cast<float *>(smem + L::off_A);
   float *sBeta = reinterpret_cast<float *>(smem + L::off_beta);
   float *sKdec = reinterpret_cast<float *>(smem + L::off_kdec);
+  float *sTot = reinterpret_cast<float *>(smem + L::off_tot);
   float *sGam = reinterpret_cast<float *>(smem + L::off_gam);
   T *sWt = sK;   // reuses region X once op #2 is done with the keys
   T *sUt = sVt;  // reuses region Y once op #4 has read the values
@@ -96,28 +101,66 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
   const T *qbase = static_cast<const T *>(a.q) + (size_t)start * qk_row + (size_t)hk * DK;
   const T *vbase = static_cast<const T *>(a.v) + (size_t)start * v_row + (size_t)h * DV;
 
-  // ---- stage K (token rows and channel rows) and V (channel rows)
-  for (int idx = tid; idx < kChunk * DK / V; idx += kLocalThreads) {
-    const int r = idx / (DK / V), cv = (idx % (DK / V)) * V;
-    uint4 u = make_uint4(0, 0, 0, 0);
-    if (r < len) u = *reinterpret_cast<const uint4 *>(kbase + (size_t)r * qk_row + cv);
-    *reinterpret_cast<uint4 *>(sK + r * L::LDK + cv) = u;
+  // ---- every global load first: this wave's queries (op #2 operand), the
+  //      chunk's keys, values and gates (padded tokens: zeros)
+  const int rq = 16 * wave + col;  // token this lane feeds as a column of A^T and P^T
+  Frag<T> qf[DK / 32];
 #pragma unroll
-    for (int j = 0; j < V; ++j) sKt[(cv + j) * L::LDT + r] = Vec16<T>::raw(u, j);
-  }
-  for (int idx = tid; idx < kChunk * DV / V; idx += kLocalThreads) {
-    const int r = idx / (DV / V), cv = (idx % (DV / V)) * V;
-    uint4 u = make_uint4(0, 0, 0, 0);
-    if (r < len) u = *reinterpret_cast<const uint4 *>(vbase + (size_t)r * v_row + cv);
+  for (int kb = 0; kb < DK / 32; ++kb)
+    qf[kb] = rq < len ? load_frag(qbase + (size_t)rq * qk_row + kb * 32, grp) : zero_frag<T>();
+  // keys and values: lane = token, wave w = channel quarter [w*D/4, (w+1)*D/4)
+  constexpr int NKV = DK / 4 / V, NVV = DV / 4 / V;  // 16-byte vectors per lane
+  u32x4 kv[NKV], vv[NVV];
 #pragma unroll
-    for (int j = 0; j < V; ++j) sVt[(cv + j) * L::LDT + r] = Vec16<T>::raw(u, j);
+  for (int it = 0; it < NKV; ++it)
+    kv[it] = lane < len ? *reinterpret_cast<const u32x4 *>(kbase + (size_t)lane * qk_row + wave * (DK / 4) + it * V)
+                        : u32x4{0, 0, 0, 0};
+#pragma unroll
+  for (int it = 0; it < NVV; ++it)
+    vv[it] = lane < len ? *reinterpret_cast<const u32x4 *>(vbase + (size_t)lane * v_row + wave * (DV / 4) + it * V)
+                        : u32x4{0, 0, 0, 0};
+  // this lane's queries in accumulator layout (channels 16m + 4grp .. +3), for Q'
+  f32x4 qacc[KT];
+#pragma unroll
+  for (int m = 0; m < KT; ++m) qacc[m] = rq < len ? load4(qbase + (size_t)rq * qk_row + 16 * m + 4 * grp) : zero4();
+  const float bval = (tid < kChunk && tid < len) ? a.beta[(size_t)(start + tid) * a.Hv + h] : 0.f;
+  constexpr int GPT = KDA ? kChunk * DK / kLocalThreads : 1;  // KDA: gate values per thread
+  float gk[GPT];
+  if constexpr (KDA) {
+    // thread = (channel d, token segment): GPT consecutive tokens of one channel
+    const int d = tid % DK, seg = tid / DK;
+    const float *gb = a.g + ((size_t)start * a.Hv + h) * DK + d;
+#pragma unroll
+    for (int u = 0; u < GPT; ++u) {
+      const int r = seg * GPT + u;
+      gk[u] = r < len ? gb[(size_t)r * a.Hv * DK] : 0.f;
+    }
+  } else {
+    gk[0] = (tid < kChunk && tid < len) ? a.g[(size_t)(start + tid) * a.Hv + h] : 0.f;
   }
 
-  // ---- op #1: beta and gamma (padded tokens: g = 0, b = 0)
-  if (tid < kChunk) sBeta[tid] = tid < len ? a.beta[(size_t)(start + tid) * a.Hv + h] : 0.f;
+  // ---- stage K (token rows and channel rows) and V (channel rows); the
+  //      channel-row writes of one wave cover 64 consecutive tokens of one row
+#pragma unroll
+  for (int it = 0; it < NKV; ++it) {
+    const int cv = wave * (DK / 4) + it * V;
+    const uint4 u = __builtin_bit_cast(uint4, kv[it]);
+    *reinterpret_cast<uint4 *>(sK + lane * L::LDK + cv) = u;
+#pragma unroll
+    for (int j = 0; j < V; ++j) sKt[(cv + j) * L::LDT + lane] = V16::raw(u, j);
+  }
+#pragma unroll
+  for (int it = 0; it < NVV; ++it) {
+    const int cv = wave * (DV / 4) + it * V;
+    const uint4 u = __builtin_bit_cast(uint4, vv[it]);
+#pragma unroll
+    for (int j = 0; j < V; ++j) sVt[(cv + j) * L::LDT + lane] = V16::raw(u, j);
+  }
+  // ---- op #1: beta and gamma (inclusive cumulative log-gate)
+  if (tid < kChunk) sBeta[tid] = bval;
   if constexpr (!KDA) {
     if (wave == 0) {
-      float x = lane < len ? a.g[(size_t)(start + lane) * a.Hv + h] : 0.f;
+      float x = gk[0];
 #pragma unroll
       for (int off = 1; off < 64; off <<= 1) {
         const float y = __shfl_up(x, off);
@@ -126,172 +169,172 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       sGam[lane] = x;
     }
   } else {
-    const float *gb = a.g + ((size_t)start * a.Hv + h) * DK;
-    const size_t g_row = (size_t)a.Hv * DK;
-    for (int d = tid; d < DK; d += kLocalThreads) {
-      float acc = 0.f;
-#pragma unroll 8
-      for (int r = 0; r < kChunk; ++r) {
-        if (r < len) acc += gb[(size_t)r * g_row + d];
-        sGam[r * L::LDG + d] = acc;
-      }
-    }
+    // segment-local scan in registers, then add the totals of earlier segments
+    const int d = tid % DK, seg = tid / DK;
+#pragma unroll
+    for (int u = 1; u < GPT; ++u) gk[u] += gk[u - 1];
+    sTot[seg * DK + d] = gk[GPT - 1];
+    __syncthreads();
+    float off = 0.f;
+    for (int s2 = 0; s2 < seg; ++s2) off += sTot[s2 * DK + d];
+#pragma unroll
+    for (int u = 0; u < GPT; ++u) sGam[(seg * GPT + u) * L::LDG + d] = gk[u] + off;
   }
   __syncthreads();
 
-  // ---- op #2: A (into LDS) and P (to the workspace); wave i = row block i
-  T *Pout = static_cast<T *>(a.P) + blk * (kChunk * kChunk);
+  // ---- op #2, transposed: wave i owns tokens r in [16i, 16i+16) as the
+  //      columns of A^T and P^T and computes the row blocks s = 16j.. (j <= i).
+  //      A goes to LDS row-major (A[r][s], 4 consecutive s per lane); the P^T
+  //      accumulators stay in registers: two of them form the P^T fragment of
+  //      a 32-token k-block (accumulator slot map), the B operand of Q' and O_loc.
+  f32x4 accP[4];
   {
-    const int i = wave, r0 = 16 * i, ra = r0 + col;
-    const T *qrow = qbase + (size_t)ra * qk_row;
-    if constexpr (!KDA) {
-      Frag<T> ka[DK / 32], qa[DK / 32];
+    const int i = wave, r = rq;
+    f32x4 accA[4];
 #pragma unroll
-      for (int kb = 0; kb < DK / 32; ++kb) {
-        ka[kb] = load_frag(sK + ra * L::LDK + kb * 32, grp);
-        qa[kb] = ra < len ? load_frag(qrow + kb * 32, grp) : zero_frag<T>();
-      }
+    for (int j = 0; j < 4; ++j) accA[j] = accP[j] = zero4();
+    if constexpr (!KDA) {
+      Frag<T> kr[DK / 32];
+#pragma unroll
+      for (int kb = 0; kb < DK / 32; ++kb) kr[kb] = load_frag(sK + r * L::LDK + kb * 32, grp);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        f32x4 accA = zero4(), accP = zero4();
         if (j <= i) {
 #pragma unroll
           for (int kb = 0; kb < DK / 32; ++kb) {
-            const Frag<T> kf = load_frag(sK + (16 * j + col) * L::LDK + kb * 32, grp);
-            accA = mma(accA, ka[kb], kf);
-            accP = mma(accP, qa[kb], kf);
+            const Frag<T> ks = load_frag(sK + (16 * j + col) * L::LDK + kb * 32, grp);
+            accA[j] = mma(accA[j], ks, kr[kb]);
+            accP[j] = mma(accP[j], ks, qf[kb]);
           }
         }
-        const int s = 16 * j + col;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int r = r0 + 4 * grp + e;
-          float vA = 0.f, vP = 0.f;
-          if (s <= r) {
-            const float dec = __expf(sGam[r] - sGam[s]);
-            vP = accP[e] * dec;
-            if (s < r) vA = sBeta[r] * accA[e] * dec;
-          }
-          sA[r * L::LDA + s] = vA;
-          Pout[r * kChunk + s] = E::from_f32(vP);
+          const int s = 16 * j + 4 * grp + e;
+          const float dec = s <= r ? __expf(sGam[r] - sGam[s]) : 0.f;
+          accA[j][e] = s < r ? sBeta[r] * accA[j][e] * dec : 0.f;
+          accP[j][e] = accP[j][e] * dec;
         }
+        *reinterpret_cast<f32x4 *>(sA + r * L::LDA + 16 * j + 4 * grp) = accA[j];
       }
     } else {
-      const int rho = r0;  // reference token of this row block
-      Frag<T> ka[DK / 32], qa[DK / 32];
+      const int rho = 16 * i;  // reference token: first token of this wave's block
+      // B operands (token r side): k_r e^(gamma_r - gamma_rho), q_r e^(gamma_r - gamma_rho)
+      Frag<T> kr[DK / 32], qr[DK / 32];
 #pragma unroll
       for (int kb = 0; kb < DK / 32; ++kb) {
         float xk[8], xq[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int d = kb * 32 + kc(grp, j);
-          const float ex = __expf(sGam[ra * L::LDG + d] - sGam[rho * L::LDG + d]);
-          xk[j] = E::to_f32(sK[ra * L::LDK + d]) * ex;
-          xq[j] = ra < len ? E::to_f32(qrow[d]) * ex : 0.f;
+        for (int jj = 0; jj < 8; ++jj) {
+          const int d = kb * 32 + kc(grp, jj);
+          const float ex = __expf(sGam[r * L::LDG + d] - sGam[rho * L::LDG + d]);
+          xk[jj] = E::to_f32(sK[r * L::LDK + d]) * ex;
+          xq[jj] = frag_elem(qf[kb], jj) * ex;
         }
-        ka[kb] = make_frag<T>(xk);
-        qa[kb] = make_frag<T>(xq);
+        kr[kb] = make_frag<T>(xk);
+        qr[kb] = make_frag<T>(xq);
       }
-      for (int j = 0; j < i; ++j) {  // off-diagonal blocks: factored decay
-        f32x4 accA = zero4(), accP = zero4();
+      for (int j = 0; j < i; ++j) {  // off-diagonal: factored decay, both factors <= 1
         const int sb = 16 * j + col;
 #pragma unroll
         for (int kb = 0; kb < DK / 32; ++kb) {
-          float xb[8];
+          float xs[8];
 #pragma unroll
           for (int jj = 0; jj < 8; ++jj) {
             const int d = kb * 32 + kc(grp, jj);
-            xb[jj] = E::to_f32(sK[sb * L::LDK + d]) *
-                     __expf(sGam[rho * L::LDG + d] - sGam[sb * L::LDG + d]);
+            xs[jj] = E::to_f32(sK[sb * L::LDK + d]) * __expf(sGam[rho * L::LDG + d] - sGam[sb * L::LDG + d]);
           }
-          const Frag<T> kf = make_frag<T>(xb);
-          accA = mma(accA, ka[kb], kf);
-          accP = mma(accP, qa[kb], kf);
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = r0 + 4 * grp + e;
-          sA[r * L::LDA + sb] = sBeta[r] * accA[e];
-          Pout[r * kChunk + sb] = E::from_f32(accP[e]);
+          const Frag<T> ks = make_frag<T>(xs);
+          accA[j] = mma(accA[j], ks, kr[kb]);
+          accP[j] = mma(accP[j], ks, qr[kb]);
         }
       }
-      {  // diagonal block: elementwise fp32
-        const int s = r0 + col;
-        float accA[4] = {0.f, 0.f, 0.f, 0.f}, accP[4] = {0.f, 0.f, 0.f, 0.f};
+      {  // diagonal block: elementwise fp32 (exponents clamped at 0 before masking)
+        const T *qrow = qbase + (size_t)r * qk_row;
         for (int d = 0; d < DK; ++d) {
-          const float ks = E::to_f32(sK[s * L::LDK + d]);
-          const float gs = sGam[s * L::LDG + d];
+          const float kd = E::to_f32(sK[r * L::LDK + d]);
+          const float qd = r < len ? E::to_f32(qrow[d]) : 0.f;
+          const float gr = sGam[r * L::LDG + d];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const int r = r0 + 4 * grp + e;
-            const float ex = __expf(fminf(sGam[r * L::LDG + d] - gs, 0.f));
-            const float kr = E::to_f32(sK[r * L::LDK + d]);
-            const float qr = r < len ? E::to_f32(qbase[(size_t)r * qk_row + d]) : 0.f;
-            accA[e] += kr * ks * ex;
-            accP[e] += qr * ks * ex;
+            const int s = 16 * i + 4 * grp + e;
+            const float ks = E::to_f32(sK[s * L::LDK + d]) * __expf(fminf(gr - sGam[s * L::LDG + d], 0.f));
+            accA[i][e] += kd * ks;
+            accP[i][e] += qd * ks;
           }
         }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = r0 + 4 * grp + e;
-          sA[r * L::LDA + s] = s < r ? sBeta[r] * accA[e] : 0.f;
-          Pout[r * kChunk + s] = E::from_f32(s <= r ? accP[e] : 0.f);
-        }
       }
-      for (int j = i + 1; j < 4; ++j) {  // above the diagonal: zero
-        const int s = 16 * j + col;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int r = r0 + 4 * grp + e;
-          sA[r * L::LDA + s] = 0.f;
-          Pout[r * kChunk + s] = E::from_f32(0.f);
+          const int s = 16 * j + 4 * grp + e;
+          accA[j][e] = (j <= i && s < r) ? sBeta[r] * accA[j][e] : 0.f;
+          accP[j][e] = (j <= i && s <= r) ? accP[j][e] : 0.f;
         }
+        *reinterpret_cast<f32x4 *>(sA + r * L::LDA + 16 * j + 4 * grp) = accA[j];
       }
     }
   }
   __syncthreads();
 
-  if (wave == 0) {
-    // ---- op #3: T = (I + A)^-1.  Lane j solves column j:
-    //      x_r = delta_rj - sum_{s<r} A[r][s] x_s   (rows r < j give x_r = 0)
-    float x[kChunk];
+  // ---- op #3: T = (I + A)^-1 (unit lower triangular, fp32), blocked by 16.
+  //      Diagonal blocks: wave w inverts block w by forward substitution (lane
+  //      j < 16 solves column j).  Then block rows i = 1..3: wave j < i forms
+  //      T_ij = -T_ii sum_{k=j}^{i-1} A_ik T_kj with fp32 MFMA (16x16x4), and
+  //      block row i overwrites A's block row i, which later rows never read.
+  if (lane < 16) {
+    const int b0 = 16 * wave, j = lane;
+    float x[16];
 #pragma unroll
-    for (int r = 0; r < kChunk; ++r) {
-      const float *Ar = sA + r * L::LDA;
-      float p0 = 0.f, p1 = 0.f, p2 = 0.f, p3 = 0.f;
+    for (int r = 0; r < 16; ++r) {
+      const float *Ar = sA + (b0 + r) * L::LDA + b0;
+      float acc = (r == j) ? 1.f : 0.f;
 #pragma unroll
-      for (int s = 0; s + 3 < r; s += 4) {
-        const f32x4 av = *reinterpret_cast<const f32x4 *>(Ar + s);
-        p0 += av[0] * x[s];
-        p1 += av[1] * x[s + 1];
-        p2 += av[2] * x[s + 2];
-        p3 += av[3] * x[s + 3];
-      }
-#pragma unroll
-      for (int s = r & ~3; s < r; ++s) p0 += Ar[s] * x[s];
-      x[r] = (r == lane ? 1.f : 0.f) - ((p0 + p1) + (p2 + p3));
+      for (int s = 0; s < r; ++s) acc -= Ar[s] * x[s];
+      x[r] = acc;
     }
 #pragma unroll
-    for (int r = 0; r < kChunk; ++r) sA[r * L::LDA + lane] = x[r];
-  } else {
-    // chunk decay e^gamma_last, and (GDN) each token's key decay to the chunk end
-    const int t2 = tid - 64;
-    float *dec_out = a.dec + blk * DK;
-    if constexpr (KDA) {
-      for (int d = t2; d < DK; d += kLocalThreads - 64)
-        dec_out[d] = __expf(sGam[(kChunk - 1) * L::LDG + d]);
-    } else {
-      if (t2 < kChunk) sKdec[t2] = __expf(sGam[kChunk - 1] - sGam[t2]);
-      if (t2 == 0) dec_out[0] = __expf(sGam[kChunk - 1]);
-    }
+    for (int r = 0; r < 16; ++r) sA[(b0 + r) * L::LDA + b0 + j] = x[r];
   }
   __syncthreads();
+#pragma unroll
+  for (int i = 1; i < 4; ++i) {
+    f32x4 res = zero4();
+    if (wave < i) {
+      const int j = wave;
+      f32x4 y = zero4();  // sum_k A_ik T_kj
+      for (int k = j; k < i; ++k) {
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+          const float av = sA[(16 * i + col) * L::LDA + 16 * k + 4 * st + grp];
+          const float tv = sA[(16 * k + 4 * st + grp) * L::LDA + 16 * j + col];
+          y = __builtin_amdgcn_mfma_f32_16x16x4f32(av, tv, y, 0, 0, 0);
+        }
+      }
+      // T_ii y: the accumulator rows 4grp + st of y are the k index of step st
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        const float tv = sA[(16 * i + col) * L::LDA + 16 * i + 4 * grp + st];
+        res = __builtin_amdgcn_mfma_f32_16x16x4f32(tv, y[st], res, 0, 0, 0);
+      }
+    }
+    __syncthreads();  // every read of block row i of A is done
+    if (wave < i) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sA[(16 * i + 4 * grp + e) * L::LDA + 16 * wave + col] = -res[e];
+    }
+    __syncthreads();
+  }
 
   // ---- op #4: wave i = token block i.  T' = T Diag(b) (GDN: also e^gamma_s).
-  // W and U~ go to LDS as channel rows: sWt[d_k][token] (region X, free since
-  // op #2), sUt[d_v][token] (region Y, once every wave has read the values).
+  //      W and U~ go to LDS as channel rows with tokens kmap-permuted inside
+  //      each 32-token block: sWt[d_k][.] over the keys (region X, free since
+  //      op #2), sUt[d_v][.] over the values once every wave has read them.
   {
     const int i = wave, r = 16 * i + col;
+    if constexpr (!KDA) {
+      if (tid < kChunk) sKdec[tid] = __expf(sGam[kChunk - 1] - sGam[tid]);
+    }
     Frag<T> tu[2], tw[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -307,17 +350,18 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       tu[kb] = make_frag<T>(xu);
       tw[kb] = make_frag<T>(xw);
     }
-    // U~ rows = tokens, columns = d_v; W rows = tokens, columns = d_k
-    f32x4 accU[DV / 16];
+    f32x4 accU[VT];
 #pragma unroll
-    for (int n = 0; n < DV / 16; ++n) {
+    for (int n = 0; n < VT; ++n) {
       accU[n] = zero4();
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
         accU[n] = mma(accU[n], tu[kb], load_frag(sVt + (16 * n + col) * L::LDT + kb * 32, grp));
     }
+    // lane rows are tokens 16i + 4grp + e: slots 4(i & 1) + e of k-block i >> 1
+    const int tpos = 32 * (i >> 1) + 8 * grp + 4 * (i & 1);
 #pragma unroll
-    for (int n = 0; n < DK / 16; ++n) {
+    for (int n = 0; n < KT; ++n) {
       const int d = 16 * n + col;
       f32x4 acc = zero4();
 #pragma unroll
@@ -336,38 +380,54 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         }
         acc = mma(acc, tw[kb], kf);
       }
-      // lane: column d, rows (tokens) 16i + 4grp + e
-      store4(sWt + d * L::LDT + 16 * i + 4 * grp, acc);
+      store4(sWt + d * L::LDT + tpos, acc);
     }
-    __syncthreads();  // every wave has read sVt
+    __syncthreads();  // every wave has read sVt and sKt
 #pragma unroll
-    for (int n = 0; n < DV / 16; ++n) store4(sUt + (16 * n + col) * L::LDT + 16 * i + 4 * grp, accU[n]);
+    for (int n = 0; n < VT; ++n) store4(sUt + (16 * n + col) * L::LDT + tpos, accU[n]);
+  }
+  // ---- Kt = (K * e^(gamma_last - gamma))^T in place of the staged keys, tokens
+  //      kmap-permuted like sWt / sUt (thread d < DK owns channel row d)
+  if (tid < DK) {
+    const int d = tid;
+    uint4 row[kChunk / V];
+#pragma unroll
+    for (int u = 0; u < kChunk / V; ++u) row[u] = *reinterpret_cast<const uint4 *>(sKt + d * L::LDT + u * V);
+#pragma unroll
+    for (int u = 0; u < kChunk / V; ++u) {
+      float outv[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const int p = u * V + j;
+        const int s = (p & ~31) + kmap((p & 31) >> 3, p & 7);
+        const float ex = KDA ? __expf(sGam[(kChunk - 1) * L::LDG + d] - sGam[s * L::LDG + d]) : sKdec[s];
+        outv[j] = V16::get(row[s / V], s % V) * ex;
+      }
+      *reinterpret_cast<uint4 *>(sKt + d * L::LDT + u * V) = V16::pack(outv);
+    }
+  }
+  {  // chunk decay e^gamma_last
+    float *dec_out = a.dec + blk * DK;
+    if constexpr (KDA) {
+      if (tid < DK) dec_out[tid] = __expf(sGam[(kChunk - 1) * L::LDG + tid]);
+    } else {
+      if (tid == 0) dec_out[0] = __expf(sGam[kChunk - 1]);
+    }
   }
   __syncthreads();
 
-  // ---- reduce-side products.  Kt fragments are built from the staged keys:
-  //      Kt[d][s] = K[s][d] e^(gamma_last - gamma_s)  (KDA: per channel d)
-  constexpr int KT = DK / 16, VT = DV / 16;
-  constexpr int KPW = KT / 4;  // d_k tiles per wave
-  auto kt_frag = [&](int d, int kb) {
-    float x[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int s = kb * 32 + kc(grp, j);
-      const float ex = KDA ? __expf(sGam[(kChunk - 1) * L::LDG + d] - sGam[s * L::LDG + d]) : sKdec[s];
-      x[j] = E::to_f32(sKt[d * L::LDT + s]) * ex;
-    }
-    return make_frag<T>(x);
-  };
+  // ---- reduce-side products; every token contraction pairs kmap-permuted
+  //      LDS rows or the P^T accumulator fragments
   {
     // (a) -M = -(Kt W), the state kernel's A operand (fragment order, prefill.h).
-    //     Computed transposed, M^T = W^T Kt^T: rows d_in from sWt, columns
-    //     d_out from Kt.
+    //     Computed transposed, M^T = W^T Kt^T: rows d_in from sWt, columns d_out from Kt.
     T *nm_out = static_cast<T *>(a.NM) + blk * ((size_t)DK * DK);
 #pragma unroll
     for (int nn = 0; nn < KPW; ++nn) {
-      const int n = wave * KPW + nn, dout = 16 * n + col;  // this lane's B column
-      const Frag<T> bk[2] = {kt_frag(dout, 0), kt_frag(dout, 1)};
+      const int n = wave * KPW + nn;
+      Frag<T> bk[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) bk[kb] = load_frag(sKt + (16 * n + col) * L::LDT + kb * 32, grp);
 #pragma unroll
       for (int m = 0; m < KT; ++m) {
         f32x4 acc = zero4();
@@ -384,7 +444,9 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 #pragma unroll
     for (int mm = 0; mm < KPW; ++mm) {
       const int m = wave * KPW + mm;
-      const Frag<T> ak[2] = {kt_frag(16 * m + col, 0), kt_frag(16 * m + col, 1)};
+      Frag<T> ak[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) ak[kb] = load_frag(sKt + (16 * m + col) * L::LDT + kb * 32, grp);
 #pragma unroll
       for (int n = 0; n < VT; ++n) {
         f32x4 acc = zero4();
@@ -395,30 +457,23 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       }
     }
     // (c) Q' = Q e^gamma - P W and (d) O_loc = P U~, the output kernel's B
-    //     operand and accumulator init (fragment order, token tile nt = w);
-    //     computed transposed (rows = channels, columns = tokens 16w..16w+15).
-    //     P is causal: k-blocks kb <= w/2.
-    const int r = 16 * wave + col;
-    const T *prow = static_cast<const T *>(a.P) + blk * (kChunk * kChunk) + (size_t)r * kChunk;
-    Frag<T> bp[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) bp[kb] = load_frag(prow + kb * 32, grp);
+    //     operand and accumulator init (fragment order, token tile nt = wave),
+    //     computed transposed with this wave's P^T fragments.  P is causal:
+    //     k-blocks kb <= wave/2 only.
+    const Frag<T> pb[2] = {frag_from_acc<T>(accP[0], accP[1]), frag_from_acc<T>(accP[2], accP[3])};
     const int nkb = (wave >> 1) + 1;
+    const int r = rq;
     T *qp_out = static_cast<T *>(a.Qp) + blk * ((size_t)kChunk * DK) + (size_t)wave * (DK / 32) * 64 * 8;
-    const T *qrow = qbase + (size_t)r * qk_row;
 #pragma unroll
     for (int m = 0; m < KT; ++m) {
+      const int d = 16 * m + 4 * grp;
+      f32x4 qe = qacc[m];
       f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-        if (kb < nkb) acc = mma(acc, load_frag(sWt + (16 * m + col) * L::LDT + kb * 32, grp), bp[kb]);
-      const int d = 16 * m + 4 * grp;
-      f32x4 qe = zero4();
-      if (r < len) {
-        qe = load4(qrow + d);
+        if (kb < nkb) acc = mma(acc, load_frag(sWt + (16 * m + col) * L::LDT + kb * 32, grp), pb[kb]);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) qe[e] *= KDA ? __expf(sGam[r * L::LDG + d + e]) : __expf(sGam[r]);
-      }
+      for (int e = 0; e < 4; ++e) qe[e] *= KDA ? __expf(sGam[r * L::LDG + d + e]) : __expf(sGam[r]);
       store4(qp_out + ((size_t)(m >> 1) * 64 + lane) * 8 + 4 * (m & 1), qe - acc);
     }
     T *ol_out = static_cast<T *>(a.Ol) + blk * ((size_t)kChunk * DV) + (size_t)wave * (DV / 16) * 64 * 4;
@@ -427,7 +482,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-        if (kb < nkb) acc = mma(acc, load_frag(sUt + (16 * m + col) * L::LDT + kb * 32, grp), bp[kb]);
+        if (kb < nkb) acc = mma(acc, load_frag(sUt + (16 * m + col) * L::LDT + kb * 32, grp), pb[kb]);
       store4(ol_out + ((size_t)m * 64 + lane) * 4, acc);
     }
   }

@@ -20,7 +20,6 @@ constexpr int kChunk = 64;  // chunk length C (paper Sec. 7.1 uses C = 64)
 //   dec e^gamma_last                 (Dk floats; GDN: element 0 only)
 //   Qp  Q' = Q * e^gamma - P W       (64 x Dk)
 //   Ol  O_loc = P U~                 (64 x Dv)
-//   P   decay-masked Q K^T           (64 x 64, row-major; scratch of the first kernel)
 //   Hs  S_c, the state entering the chunk (as S^T, Dk x Dv)
 // so that  S^T_{c+1} = D S^T_c + NM S^T_c + B  and  O = scale (Q' S^T_c + O_loc).
 // NM, Bc, Qp, Ol and Hs are stored in fragment order (device.h): one 16-lane
@@ -51,7 +50,7 @@ struct PrefillArgs {
   int *status;         // [1] device status word (hagdn_device_code)
   int4 *seq_info;      // [N]  {first chunk, number of chunks, start token, length}
   int4 *chunk_info;    // [max_chunks] {sequence, start token, length, 0}; length 0 = unused
-  void *NM, *Bc, *Qp, *Ol, *P, *Hs;
+  void *NM, *Bc, *Qp, *Ol, *Hs;
   float *dec;
 };
 
