@@ -82,7 +82,20 @@ def main():
     ap.add_argument("--workload", type=int, default=1)
     ap.add_argument("--copies", type=int, default=6)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (10 times): the known-size "
+                         "reference that scales rocprofv3 FETCH_SIZE / WRITE_SIZE counts")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+        n = args.calibrate_copy * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": n * 4, "launches": 10}), flush=True)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU only: the method shards by (sequence, head) with no "
               "communication, so a multi-GPU figure would be N independent copies of this run; "

@@ -39,27 +39,35 @@ def algorithmic_bytes(T_total: int, N: int, Hqk: int, Hv: int, dk: int, dv: int,
 
 def kernel_bytes(kernel: str, T_total: int, N: int, Hqk: int, Hv: int, dk: int, dv: int,
                  elt_bytes: int, kda: bool, with_s0: bool, chunk: int = 64) -> int:
-    """Compulsory bytes of one kernel of the three-phase pipeline: every input it
-    reads and every output it writes, each counted once.  Per-chunk intermediates
-    are counted over the padded token count (whole 64-token chunks per sequence
-    bounded by T/64 + N chunks; for one full-length sequence this is T)."""
+    """Compulsory bytes of one kernel of the pipeline: every input it reads and
+    every output it writes, each counted once.  Per-chunk blocks are counted per
+    (chunk, value head); the timed workloads are single sequences with
+    T % 64 == 0, so chunks = T / 64.
+
+      chunk_index   cu_seqlens in; sequence and chunk tables out
+      chunk_local   q, k, v, gate, beta in; -M (dk x dk), B (dk x dv), Q' (64 x dk),
+                    O_loc (64 x dv) and the chunk decay out
+      state_prop    -M, B, decay, s0 in; per-chunk state snapshots (dk x dv), s_final out
+      output        snapshots, Q', O_loc in; o out
+    """
     e = elt_bytes
-    Tp = T_total  # single sequences with T % 64 == 0 (the timed workloads) have no padding
     chunks = (T_total + chunk - 1) // chunk
+    cb = chunks * Hv  # (chunk, value head) blocks
     gate = Hv * 4 * (dk if kda else 1)
     state = N * Hv * dk * dv * 4
+    dec = cb * (dk if kda else 1) * 4
     if kernel == "chunk_index":
         return (N + 1) * 4 + N * 16 + (T_total // chunk + N) * 16 + 4
     if kernel == "chunk_local":
         rd = T_total * (2 * Hqk * dk * e + Hv * dv * e + gate + Hv * 4)
-        wr = Tp * Hv * (dk + dv + dk + dk + chunk) * e + chunks * Hv * (dk if kda else 1) * 4
+        wr = cb * (dk * dk + dk * dv + chunk * dk + chunk * dv) * e + dec
         return rd + wr
     if kernel == "state_prop":
-        rd = Tp * Hv * (dk + dv + dk) * e + chunks * Hv * (dk if kda else 1) * 4
-        wr = Tp * Hv * dv * e + chunks * Hv * dk * dv * e
-        return rd + wr + state * (2 if with_s0 else 1)
+        rd = cb * (dk * dk + dk * dv) * e + dec + (state if with_s0 else 0)
+        wr = cb * dk * dv * e + state
+        return rd + wr
     if kernel == "output":
-        rd = chunks * Hv * dk * dv * e + Tp * Hv * (dk + dv + chunk) * e
+        rd = cb * (dk * dv + chunk * dk + chunk * dv) * e
         wr = T_total * Hv * dv * e
         return rd + wr
     raise KeyError(kernel)
