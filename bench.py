@@ -37,7 +37,7 @@ def kernel_source_hash(name: str) -> str:
     """Hash of the sources a kernel is built from (traffic counters go stale when they change)."""
     csrc = os.path.join(ROOT, "paper_2609_32114_amd", "csrc")
     files = {"chunk_local": "k1_chunk_local.hip", "state_prop": "k2_state_prop.hip",
-             "output": "k3_output.hip", "chunk_index": "k0_chunk_index.hip"}
+             "chunk_index": "k0_chunk_index.hip"}
     h = hashlib.sha256()
     for f in (files[name], "device.h", "prefill.h"):
         with open(os.path.join(csrc, f), "rb") as fh:

@@ -79,10 +79,9 @@ typedef enum { HAGDN_DEV_OK = 0, HAGDN_DEV_BAD_SEQLENS = 1 } hagdn_device_code;
 
 /* Bytes of device workspace gdn_prefill needs for these sizes (0 if the
  * arguments are invalid; hagdn_last_error() then says why).  The workspace
- * holds the chunk index, the chunk-local factors of operators #2-#6 (the
+ * holds the chunk index and the chunk-local factors of operators #2-#6 (the
  * state-independent parts of the per-chunk state update and output, after
- * Sec. 5's GEMM-first regrouping) and the per-chunk state snapshots S_c that
- * operator #6 reads: Dk*Dk + 2*Dk*Dv + 64*(Dk+Dv) elements plus Dk floats per
+ * Sec. 5's GEMM-first regrouping): Dk*Dk + Dk*Dv + 64*(Dk+Dv) elements plus Dk floats per
  * (chunk, value head) for chunks bounded by T/64 + N. */
 size_t gdn_prefill_workspace_size(int N, int T_total, int Hqk, int Hv, int Dk,
                                   int Dv, int dtype);

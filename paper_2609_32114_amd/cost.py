@@ -47,8 +47,7 @@ def kernel_bytes(kernel: str, T_total: int, N: int, Hqk: int, Hv: int, dk: int, 
       chunk_index   cu_seqlens in; sequence and chunk tables out
       chunk_local   q, k, v, gate, beta in; -M (dk x dk), B (dk x dv), Q' (64 x dk),
                     O_loc (64 x dv) and the chunk decay out
-      state_prop    -M, B, decay, s0 in; per-chunk state snapshots (dk x dv), s_final out
-      output        snapshots, Q', O_loc in; o out
+      state_prop    -M, B, decay, Q', O_loc, s0 in; o, s_final out (operators #5 and #6)
     """
     e = elt_bytes
     chunks = (T_total + chunk - 1) // chunk
@@ -63,11 +62,7 @@ def kernel_bytes(kernel: str, T_total: int, N: int, Hqk: int, Hv: int, dk: int, 
         wr = cb * (dk * dk + dk * dv + chunk * dk + chunk * dv) * e + dec
         return rd + wr
     if kernel == "state_prop":
-        rd = cb * (dk * dk + dk * dv) * e + dec + (state if with_s0 else 0)
-        wr = cb * dk * dv * e + state
-        return rd + wr
-    if kernel == "output":
-        rd = cb * (dk * dv + chunk * dk + chunk * dv) * e
-        wr = T_total * Hv * dv * e
+        rd = cb * (dk * dk + dk * dv + chunk * dk + chunk * dv) * e + dec + (state if with_s0 else 0)
+        wr = T_total * Hv * dv * e + state
         return rd + wr
     raise KeyError(kernel)

@@ -4,8 +4,8 @@
 // One call enqueues, in stream order:
 //   K0 chunk index   (1 workgroup)                  sequence/chunk tables + cu_seqlens check
 //   K1 chunk-local   (max_chunks x Hv workgroups)   operators #1-#4
-//   K2 state prop    (N x Hv x Dv/16 waves)         operator #5 (sequential over chunks)
-//   K3 output        (max_chunks x Hv workgroups)   operator #6
+//   K2 state prop    (N x Hv x Dv/16 workgroups)    operator #5 (sequential over chunks)
+//                                                   fused with operator #6
 // No allocation, no synchronisation, no pointer retained after return.
 #include <hip/hip_runtime.h>
 
@@ -34,16 +34,15 @@ int fail(int code, const char *fmt, ...) {
 }
 
 constexpr size_t kAlign = 256;
-constexpr int kNumKernels = 4;
-const char *const kKernelNames[kNumKernels] = {"chunk_index", "chunk_local", "state_prop",
-                                               "output"};
+constexpr int kNumKernels = 3;
+const char *const kKernelNames[kNumKernels] = {"chunk_index", "chunk_local", "state_prop"};
 
 bool mul_ok(size_t a, size_t b, size_t *out) { return !__builtin_mul_overflow(a, b, out); }
 bool add_ok(size_t a, size_t b, size_t *out) { return !__builtin_add_overflow(a, b, out); }
 
 // Byte offsets of every workspace region (each 256-byte aligned).
 struct Layout {
-  size_t status, seq_info, chunk_info, NM, Bc, Qp, Ol, dec, Hs, total;
+  size_t status, seq_info, chunk_info, NM, Bc, Qp, Ol, dec, total;
   int max_chunks;
 };
 
@@ -78,7 +77,6 @@ bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, Layout *L) {
   L->Qp = region(C * Dk, esz, blocks);
   L->Ol = region(C * Dv, esz, blocks);
   L->dec = region((size_t)Dk, sizeof(float), blocks);
-  L->Hs = region((size_t)Dv * Dk, esz, blocks);
   L->total = (off + kAlign - 1) / kAlign * kAlign;
   if (!ok) fail(HAGDN_EINVAL, "workspace size overflows");
   return ok;
@@ -162,7 +160,6 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   a.chunk_info = reinterpret_cast<int4 *>(w + L.chunk_info);
   a.NM = w + L.NM; a.Bc = w + L.Bc; a.Qp = w + L.Qp; a.Ol = w + L.Ol;
   a.dec = reinterpret_cast<float *>(w + L.dec);
-  a.Hs = w + L.Hs;
 
   hipStream_t st = static_cast<hipStream_t>(stream_);
   hipEvent_t *ev = nullptr;
@@ -178,8 +175,6 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   if ((e = mark(2)) != hipSuccess) goto hip_fail;
   if ((e = hagdn::launch_state_prop(a, bf16, kda, st)) != hipSuccess) goto hip_fail;
   if ((e = mark(3)) != hipSuccess) goto hip_fail;
-  if ((e = hagdn::launch_output(a, bf16, st)) != hipSuccess) goto hip_fail;
-  if ((e = mark(4)) != hipSuccess) goto hip_fail;
   return HAGDN_OK;
 hip_fail:
   return fail(HAGDN_EHIP, "HIP error: %s", hipGetErrorString(e));

@@ -1,6 +1,7 @@
 // k2_state_prop.hip -- the Reduce phase of chunkwise delta-rule prefill
-// (paper Sec. 2.1, operator #5 H): the only step that is sequential over
-// chunks.  One workgroup per (sequence, value head, 16-column tile of d_v).
+// (paper Sec. 2.1, operator #5 H), the only step that is sequential over
+// chunks, fused with the final Map (operator #6 O).  One workgroup per
+// (sequence, value head, 16-column tile of d_v).
 //
 // Per chunk the chunk-local kernel has reduced operator #5 to an affine map of
 // the state entering the chunk (S^T, d_k x d_v):
@@ -21,7 +22,12 @@
 //   3. after one barrier, reads the other waves' fragments and computes its
 //      rows of the next state: acc = D*S + B (fp32), acc += NM[rows][:] S_c.
 // Chunk-first order (paper Sec. 5, "Cross-Chunk"): S_c is read by everything
-// that needs it (snapshot, the product) before its rows are overwritten.
+// that needs it before its rows are overwritten -- including operator #6.
+// After the exchange every wave holds all of S_c (this tile's 16 columns) as
+// MFMA fragments, which are also the A operand of the output product
+//     O^T = S_c Q'^T + O_loc^T        (operator #6, factors from the chunk-local kernel)
+// so wave w emits its 16-token tile(s) of o in the same step, off the state's
+// critical path.  The state is never written to memory between chunks.
 //
 // Latency: NM rows, the B tile and the decay do not depend on the state, so
 // each wave keeps D chunks of them in flight in registers.  Loads are issued
@@ -57,15 +63,24 @@ template <typename T> struct Raw4;
 template <> struct Raw4<bf16_t> { using type = uint2; };
 template <> struct Raw4<float> { using type = f32x4; };
 
-// One chunk's state-independent operands, for the rows one wave owns.
+// One chunk's state-independent operands for the rows one wave owns (the
+// state update, on the critical path) ...
 template <typename T, int DK, bool KDA>
 struct StepOps {
   Frag<T> nm[2][DK / 32];         // NM rows 32w + 16i + col, k-block kb
   typename Raw4<T>::type b[2];    // B[32w + 16i + 4grp .. +3][dv]
   f32x4 dec[2];                   // decay of those rows (GDN: dec[0][0] only)
 };
+// ... and for the token tiles one wave outputs (off the critical path).
+template <typename T, int DK>
+struct OutOps {
+  static constexpr int TPW = 4 / (DK / 32);  // output token tiles per wave
+  Frag<T> qp[TPW][DK / 32];       // Q' block (token tile, kb): columns = tokens
+  typename Raw4<T>::type ol[TPW]; // O_loc block (token tile, this d_v tile)
+};
 
-template <typename T> constexpr int pipe_depth() { return 4; }
+// chunks of state operands in flight (a multiple of the output ring's 2)
+template <typename T> constexpr int pipe_depth() { return sizeof(T) == 2 ? 4 : 2; }
 
 template <typename T, int DK, int DV, bool KDA>
 __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs a) {
@@ -99,7 +114,9 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
     const T *__restrict__ NMg = static_cast<const T *>(a.NM);
     const T *__restrict__ Bg = static_cast<const T *>(a.Bc);
     const float *__restrict__ decg = a.dec;
-    T *__restrict__ Hsg = static_cast<T *>(a.Hs);
+    const T *__restrict__ Qpg = static_cast<const T *>(a.Qp);
+    const T *__restrict__ Olg = static_cast<const T *>(a.Ol);
+    T *__restrict__ Og = static_cast<T *>(a.o);
     auto load = [&](StepOps<T, DK, KDA> &op, int c) {
       const size_t blk = (size_t)(si.x + min(c, nch - 1)) * a.Hv + h;
       // fragment-order blocks (prefill.h): NM block (row tile 2w+i, kb), B block (tile, 2w+i)
@@ -119,17 +136,41 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
         op.dec[0][0] = decg[blk * DK];
       }
     };
-    auto step = [&](const StepOps<T, DK, KDA> &op, int c) {
-      const size_t blk = (size_t)(si.x + c) * a.Hv + h;
-      // 5-read: this wave's k-block of S_c, stored as the snapshot for
-      // operator #6 (fragment-order block (d_v tile, kb = w)), and the exchange
+    // output operands: token tiles nt = w + NW*u (fragment order, prefill.h)
+    auto load_out = [&](OutOps<T, DK> &oq, int c) {
+      const size_t blk = (size_t)(si.x + min(c, nch - 1)) * a.Hv + h;
+      const T *qp = Qpg + blk * ((size_t)kChunk * DK);
+      const T *ol = Olg + blk * ((size_t)kChunk * DV);
+#pragma unroll
+      for (int u = 0; u < OutOps<T, DK>::TPW; ++u) {
+        const int nt = w + NW * u;
+#pragma unroll
+        for (int kb = 0; kb < DK / 32; ++kb)
+          oq.qp[u][kb] = load_frag_at(qp + ((size_t)(nt * (DK / 32) + kb) * 64 + lane) * 8);
+        oq.ol[u] = load_raw4(ol + ((size_t)(nt * (DV / 16) + tile) * 64 + lane) * 4);
+      }
+    };
+    // output tiles of the previous chunk, stored one step late so the store
+    // never waits on MFMA results inside the chain's critical path
+    constexpr int TPW = OutOps<T, DK>::TPW;
+    f32x4 pend[TPW];
+    auto store_out = [&](int c) {
+      const int base = c * kChunk;  // first token of chunk c inside the sequence
+#pragma unroll
+      for (int u = 0; u < TPW; ++u) {
+        const int r = base + 16 * (w + NW * u) + col;
+        if (r < si.w) store4(Og + ((size_t)(si.z + r) * a.Hv + h) * DV + tile * 16 + 4 * grp, pend[u] * a.scale);
+      }
+    };
+    auto step = [&](const StepOps<T, DK, KDA> &op, const OutOps<T, DK> &oq, int c) {
+      // 5-read: this wave's k-block of S_c, published for the other waves
       const Frag<T> own = frag_from_acc<T>(H[0], H[1]);
-      store_frag_at(Hsg + blk * ((size_t)DV * DK) + ((size_t)(tile * (DK / 32) + w) * 64 + lane) * 8, own);
       xch[c & 1][w][lane] = own;
       __syncthreads();
       Frag<T> hb[NW];
 #pragma unroll
       for (int kb = 0; kb < NW; ++kb) hb[kb] = xch[c & 1][kb][lane];
+      if (c > 0) store_out(c - 1);
       // 5-update: rows of S^T_{c+1} = D S^T_c + B + NM S^T_c (two accumulation
       // chains per tile, k-blocks split even/odd, summed at the end)
       f32x4 acc0[2], acc1[2];
@@ -148,22 +189,40 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
         }
 #pragma unroll
       for (int i = 0; i < 2; ++i) H[i] = acc0[i] + acc1[i];
+      // operator #6 for token tile(s) w + NW*u: O^T = S_c Q'^T + O_loc^T (lane:
+      // token col, d_v rows 4grp .. +3 of this tile); issued after the state
+      // update so it runs while the next step converts and exchanges, stored
+      // next step
+#pragma unroll
+      for (int u = 0; u < TPW; ++u) {
+        pend[u] = raw4_to_f32(oq.ol[u]);
+#pragma unroll
+        for (int kb = 0; kb < NW; ++kb) pend[u] = mma(pend[u], hb[kb], oq.qp[u][kb]);
+      }
     };
 
     StepOps<T, DK, KDA> R[D];
+    OutOps<T, DK> Q[2];
 #pragma unroll
     for (int u = 0; u < D; ++u) load(R[u], u);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) load_out(Q[u], u);
     int c0 = 0;
     for (; c0 + D <= nch; c0 += D) {
 #pragma unroll
       for (int u = 0; u < D; ++u) {
-        step(R[u], c0 + u);
+        step(R[u], Q[u & 1], c0 + u);
         load(R[u], c0 + u + D);
+        load_out(Q[u & 1], c0 + u + 2);
       }
     }
 #pragma unroll
     for (int u = 0; u < D; ++u)
-      if (c0 + u < nch) step(R[u], c0 + u);  // uniform for the workgroup
+      if (c0 + u < nch) {  // uniform for the workgroup
+        step(R[u], Q[u & 1], c0 + u);
+        if (u + 2 < D) load_out(Q[u & 1], c0 + u + 2);
+      }
+    store_out(nch - 1);
   }
 
   if (a.s_final) {

@@ -20,9 +20,8 @@ constexpr int kChunk = 64;  // chunk length C (paper Sec. 7.1 uses C = 64)
 //   dec e^gamma_last                 (Dk floats; GDN: element 0 only)
 //   Qp  Q' = Q * e^gamma - P W       (64 x Dk)
 //   Ol  O_loc = P U~                 (64 x Dv)
-//   Hs  S_c, the state entering the chunk (as S^T, Dk x Dv)
 // so that  S^T_{c+1} = D S^T_c + NM S^T_c + B  and  O = scale (Q' S^T_c + O_loc).
-// NM, Bc, Qp, Ol and Hs are stored in fragment order (device.h): one 16-lane
+// NM, Bc, Qp and Ol are stored in fragment order (device.h): one 16-lane
 // by 32 (operands) or 16x16 (accumulators) block after another, 64 lanes x 8
 // (operand) or x 4 (accumulator) elements each, so every producer and consumer
 // moves whole blocks with contiguous 16- or 8-byte lane accesses:
@@ -30,8 +29,6 @@ constexpr int kChunk = 64;  // chunk length C (paper Sec. 7.1 uses C = 64)
 //       slot j of lane (col, grp) = NM[16t + col][32kb + kmap(grp, j)]
 //   Bc  accumulator blocks (d_v tile n, d_k tile m), n-major;
 //       element e of lane (col, grp) = B[16m + 4grp + e][16n + col]
-//   Hs  operand blocks (d_v tile n, k-block kb of d_k), n-major;
-//       slot j of lane (col, grp) = S^T[32kb + kmap(grp, j)][16n + col]
 //   Qp  operand blocks (token tile nt, k-block kb of d_k), nt-major;
 //       slot j of lane (col, grp) = Q'[16nt + col][32kb + kmap(grp, j)]
 //   Ol  accumulator blocks (token tile nt, d_v tile m), nt-major;
@@ -50,7 +47,7 @@ struct PrefillArgs {
   int *status;         // [1] device status word (hagdn_device_code)
   int4 *seq_info;      // [N]  {first chunk, number of chunks, start token, length}
   int4 *chunk_info;    // [max_chunks] {sequence, start token, length, 0}; length 0 = unused
-  void *NM, *Bc, *Qp, *Ol, *Hs;
+  void *NM, *Bc, *Qp, *Ol;
   float *dec;
 };
 
@@ -58,7 +55,6 @@ struct PrefillArgs {
 // (dtype, Dk, Dv, gate kind) and enqueues on `stream`.
 hipError_t launch_chunk_index(const PrefillArgs &a, hipStream_t stream);
 hipError_t launch_chunk_local(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
-hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
-hipError_t launch_output(const PrefillArgs &a, bool bf16, hipStream_t stream);
+hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);  // ops #5 + #6
 
 }  // namespace hagdn
