@@ -2,15 +2,18 @@
 """Throughput of GDN prefill on one MI355X: tokens/s, roofline fraction, CPU oracle beside it.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload 1] [--no-cpu-baseline]
+                    [--segment-chunks L]
 
-One step = one full gdn_prefill call (chunk index, chunk-local, state
-propagation, output) over the workload: by default one sequence of 4096
+One step = one full gdn_prefill call (chunk index, chunk-local, segment maps,
+state propagation with output) over the workload: by default one sequence of 4096
 tokens, 16 heads, head dim 128, bf16 q/k/v, fp32 gates and state (seeded
 synthetic inputs, see paper_2609_32114_amd/inputs.py).  Inputs are resident in
 HBM before timing; the step cycles through several input copies (more bytes
 than the 256 MB Infinity Cache) so each step reads its inputs from HBM, not
-from cache.  Per-kernel times come from HIP events recorded by the library on
-the launch stream inside the timed region.
+from cache.  The timed region holds only the K steps; per-kernel times come
+from HIP events the library records on the launch stream around each kernel
+during a second pass over the same K steps (events inside the timed region
+would add their own GPU time, about 3 us each, to every step).
 
 Prints ONE JSON line.
 """
@@ -36,10 +39,11 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 def kernel_source_hash(name: str) -> str:
     """Hash of the sources a kernel is built from (traffic counters go stale when they change)."""
     csrc = os.path.join(ROOT, "paper_2609_32114_amd", "csrc")
-    files = {"chunk_local": "k1_chunk_local.hip", "state_prop": "k2_state_prop.hip",
-             "chunk_index": "k0_chunk_index.hip"}
+    files = {"chunk_local": ("k1_chunk_local.hip",),
+             "state_prop": ("k2_state_prop.hip", "k3_segments.hip"),
+             "seg_transfer": ("k3_segments.hip",), "chunk_index": ("k0_chunk_index.hip",)}
     h = hashlib.sha256()
-    for f in (files[name], "device.h", "prefill.h"):
+    for f in files[name] + ("device.h", "prefill.h"):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -82,6 +86,8 @@ def main():
     ap.add_argument("--workload", type=int, default=1)
     ap.add_argument("--copies", type=int, default=6)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--segment-chunks", type=int, default=0,
+                    help="segment length of the state chain in 64-token chunks (0: automatic)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (10 times): the known-size "
                          "reference that scales rocprofv3 FETCH_SIZE / WRITE_SIZE counts")
@@ -110,6 +116,7 @@ def main():
     from paper_2609_32114_amd.inputs import WORKLOADS, make_workload
 
     P.load_library()
+    P.set_segment_chunks(args.segment_chunks)
     wl = WORKLOADS[args.workload]
     inp = make_workload(args.workload)
     kda = inp.kind == "kda"
@@ -143,7 +150,9 @@ def main():
         step(i)
     torch.cuda.synchronize()
 
-    P.profile_begin(args.steps)
+    # timed region: K steps bracketed by events on torch's stream (the library
+    # launches on it); no per-kernel events inside, they would add their own
+    # GPU time to the step
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
@@ -151,12 +160,19 @@ def main():
         step(args.warmup + i)
     end.record()
     torch.cuda.synchronize()
-    kernel_ms, ncalls = P.profile_end()
     ms = start.elapsed_time(end) / args.steps
+    # the same K steps again with the library's HIP events around every kernel
+    # (on the launch stream): per-kernel durations for the roofline
+    P.profile_begin(args.steps)
+    for i in range(args.steps):
+        step(args.warmup + i)
+    kernel_ms, ncalls = P.profile_end()
 
     value = T / (ms * 1e-3)
     dom = max(kernel_ms, key=kernel_ms.get)
-    dom_bytes = cost.kernel_bytes(dom, T, N, Hqk, Hv, Dk, Dv, esz, kda, inp.s0 is not None)
+    L = P.segment_chunks(N, T, Hv, Dv)
+    dom_bytes = cost.kernel_bytes(dom, T, N, Hqk, Hv, Dk, Dv, esz, kda, inp.s0 is not None,
+                                  seg_chunks=L)
     dom_ms = kernel_ms[dom]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     traffic = measured_traffic(dom, wl.name)
@@ -177,7 +193,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "kind": inp.kind, "sequences": N, "seq_len": T,
                    "q_k_heads": Hqk, "v_heads": Hv, "head_dim_k": Dk, "head_dim_v": Dv,
-                   "chunk": 64, "input_copies": len(copies)},
+                   "chunk": 64, "segment_chunks": L, "input_copies": len(copies)},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "bytes_per_launch": dom_bytes, "kernel_ms": dom_ms},

@@ -79,10 +79,15 @@ typedef enum { HAGDN_DEV_OK = 0, HAGDN_DEV_BAD_SEQLENS = 1 } hagdn_device_code;
 
 /* Bytes of device workspace gdn_prefill needs for these sizes (0 if the
  * arguments are invalid; hagdn_last_error() then says why).  The workspace
- * holds the chunk index and the chunk-local factors of operators #2-#6 (the
- * state-independent parts of the per-chunk state update and output, after
- * Sec. 5's GEMM-first regrouping): Dk*Dk + Dk*Dv + 64*(Dk+Dv) elements plus Dk floats per
- * (chunk, value head) for chunks bounded by T/64 + N. */
+ * holds the chunk and segment tables and the chunk-local factors of operators
+ * #2-#6 (the state-independent parts of the per-chunk state update and output,
+ * after Sec. 5's GEMM-first regrouping): Dk*Dk + Dk*Dv + 64*(Dk+Dv) elements
+ * plus Dk floats per (chunk, value head) for chunks bounded by T/64 + N.  When
+ * a sequence can span more than one segment of the state chain (Sec. 4's
+ * Chunk-Seg-Seg mapping; see hagdn_segment_chunks) it also holds one segment
+ * map, Dk*Dk elements plus Dk*Dv floats, per (segment, value head) for
+ * segments bounded by (T/64 + N) / L + N.  The size depends on the segment
+ * length L in force (hagdn_set_segment_chunks): query it after setting. */
 size_t gdn_prefill_workspace_size(int N, int T_total, int Hqk, int Hv, int Dk,
                                   int Dv, int dtype);
 
@@ -130,6 +135,21 @@ const char *hagdn_kernel_name(int i);
 
 /* Library version: major * 10000 + minor * 100 + patch. */
 int hagdn_version(void);
+
+/* Segment length L of the state chain, in 64-token chunks (Sec. 4's
+ * Chunk-Seg-Seg mapping).  Each sequence's chunks are cut into segments of L;
+ * the composed affine map of every segment but the last is computed in
+ * parallel, then each segment walks its own chunks from the state the earlier
+ * segments' maps give.  Results are the same for every L up to rounding
+ * order.  hagdn_set_segment_chunks(0) restores the automatic choice (a
+ * function of T_total); a positive value forces L for every later call in the
+ * process.  Not synchronised with calls in flight on other host threads: set
+ * it before querying workspace sizes.  Returns HAGDN_OK or HAGDN_EINVAL
+ * (chunks < 0 or > 2^20). */
+int hagdn_set_segment_chunks(int chunks);
+
+/* L that a call with these sizes would use now; -1 on invalid sizes. */
+int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv);
 
 #ifdef __cplusplus
 }

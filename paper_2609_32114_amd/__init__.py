@@ -23,7 +23,8 @@ import ctypes
 import os
 
 __all__ = ["gdn_prefill", "kda_prefill", "workspace_size", "device_status", "library_path",
-           "load_library", "profile_begin", "profile_end", "kernel_names", "HagdnError"]
+           "load_library", "profile_begin", "profile_end", "kernel_names", "set_segment_chunks",
+           "segment_chunks", "HagdnError"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libhagdn.so")
@@ -51,6 +52,8 @@ _SYMBOLS = {
     "hagdn_kernel_count": (ctypes.c_int, []),
     "hagdn_kernel_name": (ctypes.c_char_p, [ctypes.c_int]),
     "hagdn_version": (ctypes.c_int, []),
+    "hagdn_set_segment_chunks": (ctypes.c_int, [ctypes.c_int]),
+    "hagdn_segment_chunks": (ctypes.c_int, [ctypes.c_int] * 4),
 }
 
 
@@ -183,6 +186,25 @@ def device_status(workspace) -> int:
     if rc != 0:
         raise HagdnError(rc, _err(lib))
     return code.value
+
+
+def set_segment_chunks(chunks: int):
+    """Force the state chain's segment length (in 64-token chunks) for every later
+    call in this process; 0 restores the automatic choice.  Workspace sizes
+    depend on it: query them after setting."""
+    lib = load_library()
+    rc = lib.hagdn_set_segment_chunks(int(chunks))
+    if rc != 0:
+        raise HagdnError(rc, _err(lib))
+
+
+def segment_chunks(N: int, T: int, Hv: int, Dv: int) -> int:
+    """Segment length a call with these sizes would use now."""
+    lib = load_library()
+    L = lib.hagdn_segment_chunks(int(N), int(T), int(Hv), int(Dv))
+    if L < 0:
+        raise HagdnError(1, _err(lib))
+    return L
 
 
 def kernel_names():

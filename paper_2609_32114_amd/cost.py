@@ -38,31 +38,42 @@ def algorithmic_bytes(T_total: int, N: int, Hqk: int, Hv: int, dk: int, dv: int,
 
 
 def kernel_bytes(kernel: str, T_total: int, N: int, Hqk: int, Hv: int, dk: int, dv: int,
-                 elt_bytes: int, kda: bool, with_s0: bool, chunk: int = 64) -> int:
+                 elt_bytes: int, kda: bool, with_s0: bool, chunk: int = 64, seg_chunks: int = 0) -> int:
     """Compulsory bytes of one kernel of the pipeline: every input it reads and
     every output it writes, each counted once.  Per-chunk blocks are counted per
     (chunk, value head); the timed workloads are single sequences with
-    T % 64 == 0, so chunks = T / 64.
+    T % 64 == 0, so chunks = T / 64, cut into segments of seg_chunks chunks
+    (0: one segment).
 
-      chunk_index   cu_seqlens in; sequence and chunk tables out
+      chunk_index   cu_seqlens in; sequence, chunk and segment tables out
       chunk_local   q, k, v, gate, beta in; -M (dk x dk), B (dk x dv), Q' (64 x dk),
                     O_loc (64 x dv) and the chunk decay out
-      state_prop    -M, B, decay, Q', O_loc, s0 in; o, s_final out (operators #5 and #6)
+      seg_transfer  -M, B, decay of the chunks of every segment but the last in;
+                    the segment maps A (dk x dk) and B_seg (dk x dv fp32) out
+      state_prop    -M, B, decay, Q', O_loc, the segment maps and s0 in; o, s_final
+                    out (operators #5 and #6)
     """
     e = elt_bytes
     chunks = (T_total + chunk - 1) // chunk
     cb = chunks * Hv  # (chunk, value head) blocks
     gate = Hv * 4 * (dk if kda else 1)
     state = N * Hv * dk * dv * 4
-    dec = cb * (dk if kda else 1) * 4
+    decb = (dk if kda else 1) * 4           # decay bytes per block
+    L = seg_chunks if seg_chunks > 0 else max(chunks, 1)
+    segs = max(1, -(-chunks // L))
+    map_chunks = min(chunks, (segs - 1) * L)  # chunks of segments that have a map
+    maps = (segs - 1) * Hv * (dk * dk * e + dk * dv * 4)
     if kernel == "chunk_index":
-        return (N + 1) * 4 + N * 16 + (T_total // chunk + N) * 16 + 4
+        return (N + 1) * 4 + N * 16 + (T_total // chunk + N) * 16 + 4 + N * 8 + (chunks // L + N) * 16
     if kernel == "chunk_local":
         rd = T_total * (2 * Hqk * dk * e + Hv * dv * e + gate + Hv * 4)
-        wr = cb * (dk * dk + dk * dv + chunk * dk + chunk * dv) * e + dec
+        wr = cb * ((dk * dk + dk * dv + chunk * dk + chunk * dv) * e + decb)
         return rd + wr
+    if kernel == "seg_transfer":
+        return map_chunks * Hv * ((dk * dk + dk * dv) * e + decb) + maps
     if kernel == "state_prop":
-        rd = cb * (dk * dk + dk * dv + chunk * dk + chunk * dv) * e + dec + (state if with_s0 else 0)
+        rd = cb * ((dk * dk + dk * dv + chunk * dk + chunk * dv) * e + decb) + maps
+        rd += state if with_s0 else 0
         wr = T_total * Hv * dv * e + state
         return rd + wr
     raise KeyError(kernel)

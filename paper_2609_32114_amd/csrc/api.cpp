@@ -1,11 +1,17 @@
 // api.cpp -- the C ABI of include/hagdn.h: host-side argument checks,
-// workspace carving and the four launches, all on the caller's stream.
+// workspace carving and the launches, all on the caller's stream.
 //
 // One call enqueues, in stream order:
-//   K0 chunk index   (1 workgroup)                  sequence/chunk tables + cu_seqlens check
-//   K1 chunk-local   (max_chunks x Hv workgroups)   operators #1-#4
-//   K2 state prop    (N x Hv x Dv/16 workgroups)    operator #5 (sequential over chunks)
-//                                                   fused with operator #6
+//   K0 chunk index    (1 workgroup)                        sequence/chunk/segment tables,
+//                                                          cu_seqlens check
+//   K1 chunk-local    (max_chunks x Hv workgroups)         operators #1-#4
+//   then either, when a sequence can span two segments (segment-parallel path),
+//   K2 seg transfer   (max_segs x Hv x 2 workgroups)       segment maps of operator #5
+//   K3 seg state      (max_segs x Hv workgroups)           operator #5 per segment, fused
+//                                                          with operator #6
+//   or, when every sequence is one segment,
+//   K3 state prop     (N x Hv x Dv/16 workgroups)          operator #5 per chain, fused
+//                                                          with operator #6
 // No allocation, no synchronisation, no pointer retained after return.
 #include <hip/hip_runtime.h>
 
@@ -13,6 +19,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
+#include <cmath>
 #include <string>
 #include <vector>
 
@@ -34,16 +42,39 @@ int fail(int code, const char *fmt, ...) {
 }
 
 constexpr size_t kAlign = 256;
-constexpr int kNumKernels = 3;
-const char *const kKernelNames[kNumKernels] = {"chunk_index", "chunk_local", "state_prop"};
+constexpr int kNumKernels = 4;
+const char *const kKernelNames[kNumKernels] = {"chunk_index", "chunk_local", "seg_transfer", "state_prop"};
+
+// Chunks per segment of the state chain; 0 = chosen per call (seg_chunks).
+std::atomic<int> g_seg_override{0};
+constexpr int kMaxSegChunks = 1 << 20;
+
+// Segment length for a batch of N sequences over T tokens.  A chain of n
+// chunks walked whole costs n dependent steps on 8 CUs per head; cut into
+// segments of L it costs about L (segment maps) + n / L (prefix) + L (walk)
+// steps of a head-resident workgroup, each about three times as long (it
+// moves a whole head's operands through one CU), plus twice the matrix work.
+// Measured on MI355X the segments pay from about 256 chunks per sequence
+// (T = 32768: 0.40 ms against 0.57 ms at L = 32); below that every sequence
+// stays one segment.  L near sqrt(2 n) balances the three terms.
+int seg_chunks(int N, int T, int Hv, int Dv) {
+  (void)Hv; (void)Dv;
+  const int ov = g_seg_override.load(std::memory_order_relaxed);
+  if (ov > 0) return ov;
+  const long n_all = ((long)T + hagdn::kChunk - 1) / hagdn::kChunk;  // longest possible chain
+  const long n_avg = ((long)T / (N > 0 ? N : 1) + hagdn::kChunk - 1) / hagdn::kChunk;
+  if (n_avg < 256) return n_all > 0 ? (int)(n_all < kMaxSegChunks ? n_all : kMaxSegChunks) : 1;
+  const int L = (int)std::ceil(std::sqrt(2.0 * (double)n_avg));
+  return L < 32 ? 32 : L;
+}
 
 bool mul_ok(size_t a, size_t b, size_t *out) { return !__builtin_mul_overflow(a, b, out); }
 bool add_ok(size_t a, size_t b, size_t *out) { return !__builtin_add_overflow(a, b, out); }
 
 // Byte offsets of every workspace region (each 256-byte aligned).
 struct Layout {
-  size_t status, seq_info, chunk_info, NM, Bc, Qp, Ol, dec, total;
-  int max_chunks;
+  size_t status, seq_info, chunk_info, NM, Bc, Qp, Ol, dec, seq_seg, seg_info, Aseg, Bseg, total;
+  int max_chunks, seg_chunks, max_segs;
 };
 
 // Returns false (with the error set) if the sizes overflow.
@@ -54,8 +85,11 @@ bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, Layout *L) {
     return false;
   }
   L->max_chunks = (int)mc;
-  size_t blocks;  // (chunk, value head) blocks
-  if (!mul_ok(mc, (size_t)Hv, &blocks)) {
+  L->seg_chunks = seg_chunks(N, T, Hv, Dv);
+  const size_t ms = mc / (size_t)L->seg_chunks + (size_t)N;
+  L->max_segs = (int)ms;  // <= mc
+  size_t blocks, sblocks;  // (chunk, value head) and (segment, value head) blocks
+  if (!mul_ok(mc, (size_t)Hv, &blocks) || !mul_ok(ms, (size_t)Hv, &sblocks)) {
     fail(HAGDN_EINVAL, "workspace size overflows");
     return false;
   }
@@ -77,6 +111,12 @@ bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, Layout *L) {
   L->Qp = region(C * Dk, esz, blocks);
   L->Ol = region(C * Dv, esz, blocks);
   L->dec = region((size_t)Dk, sizeof(float), blocks);
+  L->seq_seg = region(1, sizeof(int2), (size_t)N);
+  L->seg_info = region(1, sizeof(int4), ms);
+  // segment maps exist only when a sequence can span two segments
+  const bool maps = (size_t)(T + hagdn::kChunk - 1) / hagdn::kChunk > (size_t)L->seg_chunks;
+  L->Aseg = region((size_t)Dk * Dk, esz, maps ? sblocks : 0);
+  L->Bseg = region((size_t)Dk * Dv, sizeof(float), maps ? sblocks : 0);
   L->total = (off + kAlign - 1) / kAlign * kAlign;
   if (!ok) fail(HAGDN_EINVAL, "workspace size overflows");
   return ok;
@@ -109,13 +149,15 @@ struct Profile {
   bool on = false;
   int max_calls = 0;
   int calls = 0;
-  std::vector<hipEvent_t> ev;  // [max_calls][kNumKernels + 1]
+  std::vector<hipEvent_t> ev;      // [max_calls][kNumKernels + 1]; ev[i + 1] ends kernel i
+  std::vector<unsigned char> ran;  // [max_calls][kNumKernels]: kernel i launched (else no end event)
 };
 thread_local Profile g_prof;
 
 void prof_release() {
   for (hipEvent_t e : g_prof.ev) (void)hipEventDestroy(e);
   g_prof.ev.clear();
+  g_prof.ran.clear();
   g_prof.on = false;
   g_prof.calls = g_prof.max_calls = 0;
 }
@@ -160,12 +202,29 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   a.chunk_info = reinterpret_cast<int4 *>(w + L.chunk_info);
   a.NM = w + L.NM; a.Bc = w + L.Bc; a.Qp = w + L.Qp; a.Ol = w + L.Ol;
   a.dec = reinterpret_cast<float *>(w + L.dec);
+  a.seg_chunks = L.seg_chunks;
+  a.max_segs = L.max_segs;
+  a.seq_seg = reinterpret_cast<int2 *>(w + L.seq_seg);
+  a.seg_info = reinterpret_cast<int4 *>(w + L.seg_info);
+  a.Aseg = w + L.Aseg;
+  a.Bseg = reinterpret_cast<float *>(w + L.Bseg);
+  const bool maps = (T + hagdn::kChunk - 1) / hagdn::kChunk > L.seg_chunks;
 
   hipStream_t st = static_cast<hipStream_t>(stream_);
   hipEvent_t *ev = nullptr;
-  if (g_prof.on && g_prof.calls < g_prof.max_calls)
-    ev = &g_prof.ev[(size_t)g_prof.calls++ * (kNumKernels + 1)];
-  auto mark = [&](int i) -> hipError_t { return ev ? hipEventRecord(ev[i], st) : hipSuccess; };
+  unsigned char *ran = nullptr;
+  if (g_prof.on && g_prof.calls < g_prof.max_calls) {
+    ev = &g_prof.ev[(size_t)g_prof.calls * (kNumKernels + 1)];
+    ran = &g_prof.ran[(size_t)g_prof.calls * kNumKernels];
+    ++g_prof.calls;
+    for (int i = 0; i < kNumKernels; ++i) ran[i] = 0;
+  }
+  // mark(i): event i (i = 0: before the first kernel; i > 0: kernel i-1 ended)
+  auto mark = [&](int i) -> hipError_t {
+    if (!ev) return hipSuccess;
+    if (i > 0) ran[i - 1] = 1;
+    return hipEventRecord(ev[i], st);
+  };
 
   hipError_t e;
   if ((e = mark(0)) != hipSuccess) goto hip_fail;
@@ -173,8 +232,14 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   if ((e = mark(1)) != hipSuccess) goto hip_fail;
   if ((e = hagdn::launch_chunk_local(a, bf16, kda, st)) != hipSuccess) goto hip_fail;
   if ((e = mark(2)) != hipSuccess) goto hip_fail;
-  if ((e = hagdn::launch_state_prop(a, bf16, kda, st)) != hipSuccess) goto hip_fail;
-  if ((e = mark(3)) != hipSuccess) goto hip_fail;
+  if (maps) {
+    if ((e = hagdn::launch_seg_transfer(a, bf16, kda, st)) != hipSuccess) goto hip_fail;
+    if ((e = mark(3)) != hipSuccess) goto hip_fail;
+  }
+  if ((e = maps ? hagdn::launch_seg_state(a, bf16, kda, st) : hagdn::launch_state_prop(a, bf16, kda, st)) !=
+      hipSuccess)
+    goto hip_fail;
+  if ((e = mark(4)) != hipSuccess) goto hip_fail;
   return HAGDN_OK;
 hip_fail:
   return fail(HAGDN_EHIP, "HIP error: %s", hipGetErrorString(e));
@@ -226,6 +291,7 @@ int hagdn_profile_begin(int max_calls) {
   if (max_calls < 1 || max_calls > (1 << 20)) return fail(HAGDN_EINVAL, "max_calls out of range");
   prof_release();
   g_prof.ev.assign((size_t)max_calls * (kNumKernels + 1), nullptr);
+  g_prof.ran.assign((size_t)max_calls * kNumKernels, 0);
   for (hipEvent_t &e : g_prof.ev) {
     hipError_t r = hipEventCreate(&e);
     if (r != hipSuccess) {
@@ -245,11 +311,15 @@ int hagdn_profile_end(double *mean_ms, int max_kernels, int *calls) {
   std::vector<double> sum(kNumKernels, 0.0);
   for (int c = 0; c < nc; ++c) {
     hipEvent_t *ev = &g_prof.ev[(size_t)c * (kNumKernels + 1)];
+    const unsigned char *ran = &g_prof.ran[(size_t)c * kNumKernels];
     hipError_t r = hipEventSynchronize(ev[kNumKernels]);
+    hipEvent_t prev = ev[0];
     for (int i = 0; i < kNumKernels && r == hipSuccess; ++i) {
+      if (!ran[i]) continue;  // not launched in this call: 0 ms
       float ms = 0.f;
-      r = hipEventElapsedTime(&ms, ev[i], ev[i + 1]);
+      r = hipEventElapsedTime(&ms, prev, ev[i + 1]);
       sum[i] += ms;
+      prev = ev[i + 1];
     }
     if (r != hipSuccess) {
       prof_release();
@@ -268,5 +338,17 @@ int hagdn_kernel_count(void) { return kNumKernels; }
 const char *hagdn_kernel_name(int i) { return (i >= 0 && i < kNumKernels) ? kKernelNames[i] : ""; }
 
 int hagdn_version(void) { return 100; }
+
+int hagdn_set_segment_chunks(int chunks) {
+  if (chunks < 0 || chunks > kMaxSegChunks)
+    return fail(HAGDN_EINVAL, "segment length %d out of range [0, %d]", chunks, kMaxSegChunks);
+  g_seg_override.store(chunks, std::memory_order_relaxed);
+  return HAGDN_OK;
+}
+
+int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv) {
+  if (N < 1 || T_total < 0 || Hv < 1 || Dv < 1) return fail(HAGDN_EINVAL, "bad shape"), -1;
+  return seg_chunks(N, T_total, Hv, Dv);
+}
 
 }  // extern "C"

@@ -74,6 +74,14 @@ __device__ __forceinline__ constexpr int kmap_pos(int i) {
   return i < 16 ? 8 * (i >> 2) + (i & 3) : 8 * ((i - 16) >> 2) + 4 + (i & 3);
 }
 
+// d_v column held by column j (0..15) of state tile n.  Tile pairs (2p, 2p+1)
+// interleave in groups of four, so the eight output values a lane computes
+// for tiles 2p and 2p+1 (rows 4grp + e of each) are eight consecutive columns
+// 32p + 8grp + 0..7: one 16-byte store.  A bijection of [0, 32p + 32).
+__device__ __forceinline__ constexpr int dv_of(int n, int j) {
+  return 32 * (n >> 1) + 8 * (j >> 2) + 4 * (n & 1) + (j & 3);
+}
+
 // ------------------------------------------------------------ 4-element I/O
 // Four consecutive elements as fp32 (8-byte load for bf16, 16-byte for fp32).
 __device__ __forceinline__ f32x4 load4(const bf16_t *p) {

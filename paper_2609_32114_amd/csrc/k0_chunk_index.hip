@@ -1,16 +1,21 @@
-// k0_chunk_index.hip -- builds the chunk table of a packed (varlen) batch on
-// the device, with no host synchronisation.
+// k0_chunk_index.hip -- builds the chunk and segment tables of a packed
+// (varlen) batch on the device, with no host synchronisation.
 //
 // Sequences are cut into chunks of 64 tokens that restart at every sequence
-// start; the last chunk of a sequence may be partial.  The table lets the
-// chunk-parallel kernels map blockIdx -> (sequence, first token, length) and
-// the sequential kernel walk one sequence's chunks.  It also checks the
+// start; the last chunk of a sequence may be partial.  Chunks are grouped into
+// segments of seg_chunks chunks per sequence (the last may be shorter; an
+// empty sequence gets one empty segment, so that every sequence has a
+// workgroup that writes its final state).  The tables let the chunk-parallel
+// kernels map blockIdx -> (sequence, first token, length) and the segment
+// kernels walk one segment's chunks.  The kernel also checks the
 // device-resident cu_seqlens (cu[0] = 0, nondecreasing, cu[N] = T); if they
-// are malformed it writes an empty table (every later kernel then does no
-// token work and stays in bounds) and records HAGDN_DEV_BAD_SEQLENS.
+// are malformed every sequence gets zero chunks and one empty segment (later
+// kernels then touch no token and write the initial state as the final one)
+// and it records HAGDN_DEV_BAD_SEQLENS.
 //
-// Bound: sum_n ceil(len_n / 64) <= floor(T / 64) + N = max_chunks, so every
-// chunk index of a valid batch fits the table the host sized.
+// Bounds: sum_n ceil(len_n / 64) <= floor(T / 64) + N = max_chunks, and
+// sum_n max(1, ceil(nch_n / L)) <= floor(max_chunks / L) + N = max_segs, so
+// every index of a valid batch fits the tables the host sized.
 #include "prefill.h"
 
 namespace hagdn {
@@ -20,9 +25,10 @@ constexpr int kIndexThreads = 256;
 __global__ __launch_bounds__(kIndexThreads) void chunk_index_kernel(PrefillArgs a) {
   const int tid = threadIdx.x;
   const int N = a.N;
+  const int L = a.seg_chunks;
   const int32_t *cu = a.cu_seqlens;
-  __shared__ int s_scan[kIndexThreads];
-  __shared__ int s_carry;
+  __shared__ int s_scan[2][kIndexThreads];
+  __shared__ int s_carry[2];
 
   int bad = 0;
   for (int n = tid; n < N; n += kIndexThreads)
@@ -30,9 +36,9 @@ __global__ __launch_bounds__(kIndexThreads) void chunk_index_kernel(PrefillArgs 
   if (tid == 0 && (cu[0] != 0 || cu[N] != a.T)) bad = 1;
   bad = __syncthreads_or(bad);
 
-  if (tid == 0) s_carry = 0;
+  if (tid < 2) s_carry[tid] = 0;
   __syncthreads();
-  // exclusive scan of per-sequence chunk counts, 256 sequences at a time
+  // exclusive scans of per-sequence chunk and segment counts, 256 sequences at a time
   for (int base = 0; base < N; base += kIndexThreads) {
     const int n = base + tid;
     int st = 0, len = 0;
@@ -41,25 +47,39 @@ __global__ __launch_bounds__(kIndexThreads) void chunk_index_kernel(PrefillArgs 
       len = cu[n + 1] - st;
     }
     const int nch = (len + kChunk - 1) / kChunk;
-    s_scan[tid] = nch;
+    const int nseg = n < N ? max(1, (nch + L - 1) / L) : 0;
+    s_scan[0][tid] = nch;
+    s_scan[1][tid] = nseg;
     __syncthreads();
     for (int off = 1; off < kIndexThreads; off <<= 1) {
-      const int add = tid >= off ? s_scan[tid - off] : 0;
+      const int add0 = tid >= off ? s_scan[0][tid - off] : 0;
+      const int add1 = tid >= off ? s_scan[1][tid - off] : 0;
       __syncthreads();
-      s_scan[tid] += add;
+      s_scan[0][tid] += add0;
+      s_scan[1][tid] += add1;
       __syncthreads();
     }
-    const int first = s_carry + s_scan[tid] - nch;
-    if (n < N) a.seq_info[n] = make_int4(first, nch, st, len);
+    if (n < N) {
+      a.seq_info[n] = make_int4(s_carry[0] + s_scan[0][tid] - nch, nch, st, len);
+      a.seq_seg[n] = make_int2(s_carry[1] + s_scan[1][tid] - nseg, nseg);
+    }
     __syncthreads();
-    if (tid == kIndexThreads - 1) s_carry += s_scan[tid];
+    if (tid == kIndexThreads - 1) {
+      s_carry[0] += s_scan[0][tid];
+      s_carry[1] += s_scan[1][tid];
+    }
     __syncthreads();
   }
-  const int total = s_carry;
+  int total = s_carry[0], total_segs = s_carry[1];
   // cannot happen for a valid batch; keeps every later index in range anyway
-  if (total > a.max_chunks) {
+  if (total > a.max_chunks || total_segs > a.max_segs) {
     bad = 1;
-    for (int n = tid; n < N; n += kIndexThreads) a.seq_info[n] = make_int4(0, 0, 0, 0);
+    total = 0;
+    total_segs = N;  // <= max_segs
+    for (int n = tid; n < N; n += kIndexThreads) {
+      a.seq_info[n] = make_int4(0, 0, 0, 0);
+      a.seq_seg[n] = make_int2(n, 1);
+    }
   }
   __threadfence_block();
   __syncthreads();
@@ -82,6 +102,24 @@ __global__ __launch_bounds__(kIndexThreads) void chunk_index_kernel(PrefillArgs 
       }
     }
     a.chunk_info[c] = info;
+  }
+  for (int sg = tid; sg < a.max_segs; sg += kIndexThreads) {
+    int4 info = make_int4(-1, 0, 0, 0);
+    if (sg < total_segs) {
+      // every sequence has >= 1 segment, so first segments strictly increase
+      int lo = 0, hi = N - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (a.seq_seg[mid].x <= sg) lo = mid; else hi = mid - 1;
+      }
+      const int2 ss = a.seq_seg[lo];
+      const int j = sg - ss.x;
+      if (j >= 0 && j < ss.y) {
+        const int4 s = a.seq_info[lo];
+        info = make_int4(lo, s.x + j * L, min(L, s.y - j * L), j);
+      }
+    }
+    a.seg_info[sg] = info;
   }
   if (tid == 0) a.status[0] = bad ? 1 : 0;
 }

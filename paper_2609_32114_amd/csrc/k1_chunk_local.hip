@@ -439,21 +439,27 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         store4(nm_out + ((size_t)(n * (DK / 32) + (m >> 1)) * 64 + lane) * 8 + 4 * (m & 1), -acc);
       }
     }
-    // (b) B = Kt U~, the state kernel's accumulator init (fragment order)
+    // (b) B = Kt U~, the state kernel's accumulator init (lane-major, prefill.h):
+    //     lane col of state tile n feeds U~ row dv_of(n, col), so the product
+    //     lands in the state's column order
     T *b_out = static_cast<T *>(a.Bc) + blk * ((size_t)DV * DK);
+    Frag<T> ak[KPW][2];
 #pragma unroll
-    for (int mm = 0; mm < KPW; ++mm) {
-      const int m = wave * KPW + mm;
-      Frag<T> ak[2];
+    for (int mm = 0; mm < KPW; ++mm)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) ak[kb] = load_frag(sKt + (16 * m + col) * L::LDT + kb * 32, grp);
+      for (int kb = 0; kb < 2; ++kb) ak[mm][kb] = load_frag(sKt + (16 * (wave * KPW + mm) + col) * L::LDT + kb * 32, grp);
 #pragma unroll
-      for (int n = 0; n < VT; ++n) {
+    for (int n = 0; n < VT; ++n) {
+      Frag<T> bu[2];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) bu[kb] = load_frag(sUt + dv_of(n, col) * L::LDT + kb * 32, grp);
+#pragma unroll
+      for (int mm = 0; mm < KPW; ++mm) {
+        const int m = wave * KPW + mm;
         f32x4 acc = zero4();
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-          acc = mma(acc, ak[kb], load_frag(sUt + (16 * n + col) * L::LDT + kb * 32, grp));
-        store4(b_out + ((size_t)(n * (DK / 16) + m) * 64 + lane) * 4, acc);
+        for (int kb = 0; kb < 2; ++kb) acc = mma(acc, ak[mm][kb], bu[kb]);
+        store4(b_out + ((size_t)n * 64 + lane) * (4 * KT) + 4 * m, acc);
       }
     }
     // (c) Q' = Q e^gamma - P W and (d) O_loc = P U~, the output kernel's B
@@ -476,14 +482,15 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       for (int e = 0; e < 4; ++e) qe[e] *= KDA ? __expf(sGam[r * L::LDG + d + e]) : __expf(sGam[r]);
       store4(qp_out + ((size_t)(m >> 1) * 64 + lane) * 8 + 4 * (m & 1), qe - acc);
     }
-    T *ol_out = static_cast<T *>(a.Ol) + blk * ((size_t)kChunk * DV) + (size_t)wave * (DV / 16) * 64 * 4;
+    // O_loc^T rows of state tile m: lane col feeds U~ row dv_of(m, col)
+    T *ol_out = static_cast<T *>(a.Ol) + blk * ((size_t)kChunk * DV);
 #pragma unroll
     for (int m = 0; m < VT; ++m) {
       f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-        if (kb < nkb) acc = mma(acc, load_frag(sUt + (16 * m + col) * L::LDT + kb * 32, grp), pb[kb]);
-      store4(ol_out + ((size_t)m * 64 + lane) * 4, acc);
+        if (kb < nkb) acc = mma(acc, load_frag(sUt + dv_of(m, col) * L::LDT + kb * 32, grp), pb[kb]);
+      store4(ol_out + ((size_t)m * 64 + lane) * 16 + 4 * wave, acc);
     }
   }
 }

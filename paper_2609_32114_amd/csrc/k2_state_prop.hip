@@ -1,7 +1,9 @@
 // k2_state_prop.hip -- the Reduce phase of chunkwise delta-rule prefill
 // (paper Sec. 2.1, operator #5 H), the only step that is sequential over
-// chunks, fused with the final Map (operator #6 O).  One workgroup per
-// (sequence, value head, 16-column tile of d_v).
+// chunks, fused with the final Map (operator #6 O), for chains walked whole.
+// One workgroup per (sequence, value head, 16-column tile of d_v); the tile's
+// columns are dv_of(tile, 0..15) (device.h).  Chains long enough to pay for
+// segment maps take the segment-parallel path of k3_segments.hip instead.
 //
 // Per chunk the chunk-local kernel has reduced operator #5 to an affine map of
 // the state entering the chunk (S^T, d_k x d_v):
@@ -95,7 +97,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
   const int n = pair / a.Hv, h = pair % a.Hv;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
-  const int dv = tile * 16 + col;  // state column this lane holds
+  const int dv = dv_of(tile, col);  // state column this lane holds
   const int row0 = 32 * w;         // first state row of this wave
   const int4 si = a.seq_info[n];   // {first chunk, chunks, start, length}
   const int nch = si.y;
@@ -119,7 +121,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
     T *__restrict__ Og = static_cast<T *>(a.o);
     auto load = [&](StepOps<T, DK, KDA> &op, int c) {
       const size_t blk = (size_t)(si.x + min(c, nch - 1)) * a.Hv + h;
-      // fragment-order blocks (prefill.h): NM block (row tile 2w+i, kb), B block (tile, 2w+i)
+      // NM block (row tile 2w+i, kb) in fragment order; B lane-major (prefill.h)
       const T *nm = NMg + blk * ((size_t)DK * DK);
       const T *bt = Bg + blk * ((size_t)DV * DK);
 #pragma unroll
@@ -127,7 +129,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
 #pragma unroll
         for (int kb = 0; kb < DK / 32; ++kb)
           op.nm[i][kb] = load_frag_at(nm + ((size_t)((2 * w + i) * (DK / 32) + kb) * 64 + lane) * 8);
-        op.b[i] = load_raw4(bt + ((size_t)(tile * (DK / 16) + 2 * w + i) * 64 + lane) * 4);
+        op.b[i] = load_raw4(bt + ((size_t)(tile * 64 + lane) * (DK / 16) + 2 * w + i) * 4);
       }
       if constexpr (KDA) {
 #pragma unroll
@@ -136,7 +138,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
         op.dec[0][0] = decg[blk * DK];
       }
     };
-    // output operands: token tiles nt = w + NW*u (fragment order, prefill.h)
+    // output operands: token tiles nt = w + NW*u (Q' fragment order, O_loc lane-major)
     auto load_out = [&](OutOps<T, DK> &oq, int c) {
       const size_t blk = (size_t)(si.x + min(c, nch - 1)) * a.Hv + h;
       const T *qp = Qpg + blk * ((size_t)kChunk * DK);
@@ -147,7 +149,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
 #pragma unroll
         for (int kb = 0; kb < DK / 32; ++kb)
           oq.qp[u][kb] = load_frag_at(qp + ((size_t)(nt * (DK / 32) + kb) * 64 + lane) * 8);
-        oq.ol[u] = load_raw4(ol + ((size_t)(nt * (DV / 16) + tile) * 64 + lane) * 4);
+        oq.ol[u] = load_raw4(ol + ((size_t)(tile * 64 + lane) * 4 + nt) * 4);
       }
     };
     // output tiles of the previous chunk, stored one step late so the store
@@ -159,7 +161,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
 #pragma unroll
       for (int u = 0; u < TPW; ++u) {
         const int r = base + 16 * (w + NW * u) + col;
-        if (r < si.w) store4(Og + ((size_t)(si.z + r) * a.Hv + h) * DV + tile * 16 + 4 * grp, pend[u] * a.scale);
+        if (r < si.w) store4(Og + ((size_t)(si.z + r) * a.Hv + h) * DV + dv_of(tile, 4 * grp), pend[u] * a.scale);
       }
     };
     auto step = [&](const StepOps<T, DK, KDA> &op, const OutOps<T, DK> &oq, int c) {

@@ -21,19 +21,29 @@ constexpr int kChunk = 64;  // chunk length C (paper Sec. 7.1 uses C = 64)
 //   Qp  Q' = Q * e^gamma - P W       (64 x Dk)
 //   Ol  O_loc = P U~                 (64 x Dv)
 // so that  S^T_{c+1} = D S^T_c + NM S^T_c + B  and  O = scale (Q' S^T_c + O_loc).
-// NM, Bc, Qp and Ol are stored in fragment order (device.h): one 16-lane
-// by 32 (operands) or 16x16 (accumulators) block after another, 64 lanes x 8
-// (operand) or x 4 (accumulator) elements each, so every producer and consumer
-// moves whole blocks with contiguous 16- or 8-byte lane accesses:
+// NM and Qp are stored in fragment order (device.h): one 16-lane by 32 operand
+// block after another, 64 lanes x 8 elements each; Bc and Ol lane-major, each
+// lane's accumulator values of one state tile contiguous, so every consumer
+// moves them with 16-byte lane accesses:
 //   NM  operand blocks (row tile t of d_k out, k-block kb of d_k in), t-major;
 //       slot j of lane (col, grp) = NM[16t + col][32kb + kmap(grp, j)]
-//   Bc  accumulator blocks (d_v tile n, d_k tile m), n-major;
-//       element e of lane (col, grp) = B[16m + 4grp + e][16n + col]
+//   Bc  per state tile n (d_v columns dv_of(n, 0..15), device.h), lane-major:
+//       element (m, e) of lane (col, grp), at ((n*64 + lane)*(Dk/16) + m)*4 + e,
+//       = B[16m + 4grp + e][dv_of(n, col)]
 //   Qp  operand blocks (token tile nt, k-block kb of d_k), nt-major;
 //       slot j of lane (col, grp) = Q'[16nt + col][32kb + kmap(grp, j)]
-//   Ol  accumulator blocks (token tile nt, d_v tile m), nt-major;
-//       element e of lane (col, grp) = O_loc[16nt + col][16m + 4grp + e]
+//   Ol  per state tile m, lane-major: element (nt, e) of lane (col, grp), at
+//       ((m*64 + lane)*4 + nt)*4 + e, = O_loc[16nt + col][dv_of(m, 4grp + e)]
 // Element type of every block is the I/O dtype (bf16 or fp32), dec is fp32.
+//
+// Segments (paper Sec. 4, the Chunk-Seg-Seg mapping): each sequence is cut into segments
+// of seg_chunks chunks (the last may be shorter; an empty sequence still has
+// one empty segment).  Composing the affine chunk maps over segment s gives
+// its segment map  S^T_out = A_s S^T_in + B_s  (d_k x d_k, d_k x d_v), per
+// (segment, value head) block:
+//   Aseg  A_s in NM's fragment order and element type
+//   Bseg  B_s fp32, in Bc's accumulator-block order
+// Only segments followed by another segment of the same sequence have one.
 struct PrefillArgs {
   const void *q, *k, *v;
   const float *g, *beta, *s0;
@@ -49,12 +59,22 @@ struct PrefillArgs {
   int4 *chunk_info;    // [max_chunks] {sequence, start token, length, 0}; length 0 = unused
   void *NM, *Bc, *Qp, *Ol;
   float *dec;
+  int seg_chunks;      // chunks per segment (>= 1)
+  int max_segs;        // upper bound on segments: max_chunks / seg_chunks + N
+  int2 *seq_seg;       // [N] {first segment, number of segments}
+  int4 *seg_info;      // [max_segs] {sequence (-1 = unused), first chunk, chunks, index in sequence}
+  void *Aseg;
+  float *Bseg;
 };
 
 // Host-side launchers, one per kernel; each picks the template instance for
 // (dtype, Dk, Dv, gate kind) and enqueues on `stream`.
 hipError_t launch_chunk_index(const PrefillArgs &a, hipStream_t stream);
 hipError_t launch_chunk_local(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
-hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);  // ops #5 + #6
+// ops #5 + #6 over whole chains (every sequence one segment)
+hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
+// segment-parallel path: segment maps, then ops #5 + #6 per segment
+hipError_t launch_seg_transfer(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
+hipError_t launch_seg_state(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
 
 }  // namespace hagdn

@@ -96,3 +96,32 @@ def test_profile_requires_begin():
     calls = ctypes.c_int()
     assert lib.hagdn_profile_end(arr, 4, ctypes.byref(calls)) == 1
     assert lib.hagdn_profile_begin(0) == 1
+
+
+def test_segment_length_knob():
+    import paper_2609_32114_amd as P
+    P.load_library()
+    try:
+        # automatic: short chains stay one segment, long ones get about sqrt(2 n)
+        assert P.segment_chunks(1, 256, 1, 64) == 4
+        assert P.segment_chunks(1, 0, 1, 64) == 1
+        assert P.segment_chunks(1, 4096, 16, 128) == 64
+        assert P.segment_chunks(1, 32768, 16, 128) == 32
+        assert P.segment_chunks(1, 131072, 16, 128) == 64   # 2048 chunks
+        assert P.segment_chunks(8, 34816, 32, 128) == 544   # short average chains: whole
+        P.set_segment_chunks(8)
+        auto = P.segment_chunks(1, 4096, 16, 128)
+        assert auto == 8
+        ws_auto = P.workspace_size("gdn", 1, 4096, 16, 16, 128, 128, P.HAGDN_BF16)  # L = 8
+        P.set_segment_chunks(2)
+        assert P.segment_chunks(1, 4096, 16, 128) == 2
+        ws_small = P.workspace_size("gdn", 1, 4096, 16, 16, 128, 128, P.HAGDN_BF16)
+        assert ws_small > ws_auto  # more segment maps
+        P.set_segment_chunks(64)   # one segment: no maps at all
+        ws_one = P.workspace_size("gdn", 1, 4096, 16, 16, 128, 128, P.HAGDN_BF16)
+        assert ws_one < ws_auto
+        with pytest.raises(P.HagdnError):
+            P.set_segment_chunks(-1)
+    finally:
+        P.set_segment_chunks(0)
+    assert P.segment_chunks(1, 4096, 16, 128) == 64
