@@ -217,7 +217,15 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         *reinterpret_cast<f32x4 *>(sA + r * L::LDA + 16 * j + 4 * grp) = accA[j];
       }
     } else {
-      const int rho = 16 * i;  // reference token: first token of this wave's block
+      // Per-channel decay e^(gamma_r - gamma_s), factored around a reference
+      // token rho in the middle of this wave's block: the r side carries
+      // e^(gamma_r - gamma_rho), the s side e^(gamma_rho - gamma_s), so every
+      // block -- the diagonal one included -- is an MFMA product.  Each factor
+      // spans at most 8 tokens of decay inside the block (|exponent| <= 8 max g,
+      // far from fp32/bf16 overflow); off-diagonal s-side factors are <= 1.
+      // Upper-triangle products of the diagonal block may overflow: they are
+      // discarded by selection below, never multiplied.
+      const int rho = 16 * i + 8;
       // B operands (token r side): k_r e^(gamma_r - gamma_rho), q_r e^(gamma_r - gamma_rho)
       Frag<T> kr[DK / 32], qr[DK / 32];
 #pragma unroll
@@ -233,33 +241,21 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         kr[kb] = make_frag<T>(xk);
         qr[kb] = make_frag<T>(xq);
       }
-      for (int j = 0; j < i; ++j) {  // off-diagonal: factored decay, both factors <= 1
-        const int sb = 16 * j + col;
 #pragma unroll
-        for (int kb = 0; kb < DK / 32; ++kb) {
-          float xs[8];
+      for (int j = 0; j < 4; ++j) {
+        if (j <= i) {  // uniform for the wave
+          const int sb = 16 * j + col;
 #pragma unroll
-          for (int jj = 0; jj < 8; ++jj) {
-            const int d = kb * 32 + kc(grp, jj);
-            xs[jj] = E::to_f32(sK[sb * L::LDK + d]) * __expf(sGam[rho * L::LDG + d] - sGam[sb * L::LDG + d]);
-          }
-          const Frag<T> ks = make_frag<T>(xs);
-          accA[j] = mma(accA[j], ks, kr[kb]);
-          accP[j] = mma(accP[j], ks, qr[kb]);
-        }
-      }
-      {  // diagonal block: elementwise fp32 (exponents clamped at 0 before masking)
-        const T *qrow = qbase + (size_t)r * qk_row;
-        for (int d = 0; d < DK; ++d) {
-          const float kd = E::to_f32(sK[r * L::LDK + d]);
-          const float qd = r < len ? E::to_f32(qrow[d]) : 0.f;
-          const float gr = sGam[r * L::LDG + d];
+          for (int kb = 0; kb < DK / 32; ++kb) {
+            float xs[8];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int s = 16 * i + 4 * grp + e;
-            const float ks = E::to_f32(sK[s * L::LDK + d]) * __expf(fminf(gr - sGam[s * L::LDG + d], 0.f));
-            accA[i][e] += kd * ks;
-            accP[i][e] += qd * ks;
+            for (int jj = 0; jj < 8; ++jj) {
+              const int d = kb * 32 + kc(grp, jj);
+              xs[jj] = E::to_f32(sK[sb * L::LDK + d]) * __expf(sGam[rho * L::LDG + d] - sGam[sb * L::LDG + d]);
+            }
+            const Frag<T> ks = make_frag<T>(xs);
+            accA[j] = mma(accA[j], ks, kr[kb]);
+            accP[j] = mma(accP[j], ks, qr[kb]);
           }
         }
       }
