@@ -27,15 +27,19 @@
 //
 // GDN's decay is a scalar per token, so K K^T and Q K^T are plain MFMA
 // products and the decay is applied in the epilogue.  KDA's per-channel decay
-// sits inside the contraction: off-diagonal 16x16 blocks factor it around the
-// first token rho of the row block, <k_r e^(gamma_r - gamma_rho),
-// k_s e^(gamma_rho - gamma_s)>, both factors <= 1; diagonal blocks are summed
-// elementwise in fp32 (their exponents are clamped at 0 before masking).
+// sits inside the contraction: every 16x16 block of row block i factors it
+// around the token rho = 16i + 8 in the middle of the block,
+// <k_r e^(gamma_r - gamma_rho), k_s e^(gamma_rho - gamma_s)>; inside the block
+// each factor spans at most 8 tokens of decay, off-diagonal s-side factors are
+// <= 1, and upper-triangle products (which may overflow) are discarded by
+// selection.
 //
 // Wave roles (4 waves): wave i computes row block i of A and P; wave 0 then
 // solves T by forward substitution (lane j owns column j) while waves 1-3
 // write the decay; wave i computes token block i of W and U~ into LDS; then
 // the four reduce-side products are split over the waves.
+#include <atomic>
+
 #include "device.h"
 #include "prefill.h"
 
@@ -65,22 +69,124 @@ struct LocalLayout {
   static constexpr size_t bytes = off_gam + sizeof(float) * kChunk * LDG;
 };
 
+// One (chunk, value head) work item: chunk c = item / Hv, head h = item % Hv.
+struct LocalItem {
+  int c, h, start, len;  // len 0: past the last chunk
+};
+__device__ __forceinline__ LocalItem local_item(const PrefillArgs &a, int item) {
+  LocalItem it{0, 0, 0, 0};
+  if (item < a.max_chunks * a.Hv) {
+    it.c = item / a.Hv;
+    it.h = item % a.Hv;
+    const int4 ci = a.chunk_info[it.c];
+    it.start = ci.y;
+    it.len = ci.z;
+  }
+  return it;
+}
+
+// Global inputs of one item, loaded one item ahead (padded tokens: zeros).
+// Every load is issued unconditionally from a row clamped into the chunk and
+// the padding is selected away afterwards, so the memory counters stay exact.
+template <typename T, int DK, int DV, bool KDA>
+struct LocalIn {
+  static constexpr int V = 16 / (int)sizeof(T);
+  static constexpr int NKV = DK / 4 / V, NVV = DV / 4 / V;       // 16-byte vectors per lane
+  static constexpr int GPT = KDA ? kChunk * DK / kLocalThreads : 1;  // gate values per thread
+  u32x4 kv[NKV], vv[NVV];  // keys, values: lane = token, wave = channel quarter
+  float bval, gk[GPT];     // beta of token tid; gates (KDA: thread = (channel, token segment))
+  Frag<T> qf[DK / 32];     // queries of token 16 wave + col, op #2 operand
+  f32x4 qacc[DK / 16];     // the same queries in accumulator layout (channels 16m + 4grp ..)
+
+  __device__ __forceinline__ void load_kvg(const PrefillArgs &a, const LocalItem &it) {
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int hk = it.h / (a.Hv / a.Hqk);
+    const int last = it.len - 1;
+    const size_t qk_row = (size_t)a.Hqk * DK, v_row = (size_t)a.Hv * DV;
+    const int rk = min(lane, last);
+    const T *kb = static_cast<const T *>(a.k) + (size_t)(it.start + rk) * qk_row + (size_t)hk * DK + wave * (DK / 4);
+    const T *vb = static_cast<const T *>(a.v) + (size_t)(it.start + rk) * v_row + (size_t)it.h * DV + wave * (DV / 4);
+    const bool live = lane < it.len;
+#pragma unroll
+    for (int i = 0; i < NKV; ++i) {
+      const u32x4 x = *reinterpret_cast<const u32x4 *>(kb + i * V);
+      kv[i] = live ? x : u32x4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int i = 0; i < NVV; ++i) {
+      const u32x4 x = *reinterpret_cast<const u32x4 *>(vb + i * V);
+      vv[i] = live ? x : u32x4{0, 0, 0, 0};
+    }
+    const int rt = min(tid & (kChunk - 1), last);
+    const float b = a.beta[(size_t)(it.start + rt) * a.Hv + it.h];
+    bval = (tid < kChunk && tid < it.len) ? b : 0.f;
+    if constexpr (KDA) {
+      const int d = tid % DK, seg = tid / DK;
+      const float *gb = a.g + ((size_t)it.start * a.Hv + it.h) * DK + d;
+#pragma unroll
+      for (int u = 0; u < GPT; ++u) {
+        const int r = seg * GPT + u;
+        const float x = gb[(size_t)min(r, last) * a.Hv * DK];
+        gk[u] = r < it.len ? x : 0.f;
+      }
+    } else {
+      const float x = a.g[(size_t)(it.start + rt) * a.Hv + it.h];
+      gk[0] = (tid < kChunk && tid < it.len) ? x : 0.f;
+    }
+  }
+  __device__ __forceinline__ void load_q(const PrefillArgs &a, const LocalItem &it) {
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int col = lane & 15, grp = lane >> 4;
+    const int rq = 16 * wave + col;
+    const int hk = it.h / (a.Hv / a.Hqk);
+    const size_t qk_row = (size_t)a.Hqk * DK;
+    const T *qrow = static_cast<const T *>(a.q) + (size_t)(it.start + min(rq, it.len - 1)) * qk_row + (size_t)hk * DK;
+    const bool live = rq < it.len;
+#pragma unroll
+    for (int kb = 0; kb < DK / 32; ++kb) {
+      const Frag<T> x = load_frag(qrow + kb * 32, grp);
+      qf[kb] = live ? x : zero_frag<T>();
+    }
+#pragma unroll
+    for (int m = 0; m < DK / 16; ++m) {
+      const f32x4 x = load4(qrow + 16 * m + 4 * grp);
+      qacc[m] = live ? x : zero4();
+    }
+  }
+};
+
+// Persistent where registers allow two workgroups per CU alongside the
+// next item's inputs (GDN bf16): workgroup b takes items b, b + gridDim.x, ...
+// (chunk-major, so past the last chunk every later item is empty too) and
+// loads item n+1's inputs while it computes item n.  Otherwise one workgroup
+// per item.
+template <typename T, bool KDA>
+constexpr bool local_persistent() { return !KDA && sizeof(T) == 2; }
+
 template <typename T, int DK, int DV, bool KDA>
 __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs a) {
   using L = LocalLayout<T, DK, DV, KDA>;
   using E = Elt<T>;
   using V16 = Vec16<T>;
+  using In = LocalIn<T, DK, DV, KDA>;
   constexpr int V = 16 / (int)sizeof(T);  // elements per 16-byte vector
   constexpr int KT = DK / 16, VT = DV / 16;
   constexpr int KPW = KT / 4;             // d_k tiles per wave in the reduce-side products
-  const int c = blockIdx.x, h = blockIdx.y;
-  const int4 ci = a.chunk_info[c];
-  const int len = ci.z;
-  if (len <= 0) return;
-  const int start = ci.y;
-  const int hk = h / (a.Hv / a.Hqk);
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
+  constexpr bool kKvgAhead = local_persistent<T, KDA>();
+  constexpr bool kQAhead = local_persistent<T, KDA>();
+  int item = blockIdx.x;
+  LocalItem cur = local_item(a, item);
+  if (cur.len <= 0) return;
+  In in;
+  if constexpr (kKvgAhead) in.load_kvg(a, cur);
+  if constexpr (kQAhead) in.load_q(a, cur);
+  for (;;) {
+  const LocalItem nxt = local_item(a, item + gridDim.x);
+  if constexpr (!kKvgAhead) in.load_kvg(a, cur);
+  if constexpr (!kQAhead) in.load_q(a, cur);
+  const int c = cur.c, h = cur.h, start = cur.start, len = cur.len;
   const size_t blk = (size_t)c * a.Hv + h;
 
   extern __shared__ __align__(16) unsigned char smem[];
@@ -95,49 +201,14 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
   T *sWt = sK;   // reuses region X once op #2 is done with the keys
   T *sUt = sVt;  // reuses region Y once op #4 has read the values
 
-  const size_t qk_row = (size_t)a.Hqk * DK;  // token stride of q and k
-  const size_t v_row = (size_t)a.Hv * DV;
-  const T *kbase = static_cast<const T *>(a.k) + (size_t)start * qk_row + (size_t)hk * DK;
-  const T *qbase = static_cast<const T *>(a.q) + (size_t)start * qk_row + (size_t)hk * DK;
-  const T *vbase = static_cast<const T *>(a.v) + (size_t)start * v_row + (size_t)h * DV;
-
-  // ---- every global load first: this wave's queries (op #2 operand), the
-  //      chunk's keys, values and gates (padded tokens: zeros)
   const int rq = 16 * wave + col;  // token this lane feeds as a column of A^T and P^T
-  Frag<T> qf[DK / 32];
-#pragma unroll
-  for (int kb = 0; kb < DK / 32; ++kb)
-    qf[kb] = rq < len ? load_frag(qbase + (size_t)rq * qk_row + kb * 32, grp) : zero_frag<T>();
-  // keys and values: lane = token, wave w = channel quarter [w*D/4, (w+1)*D/4)
-  constexpr int NKV = DK / 4 / V, NVV = DV / 4 / V;  // 16-byte vectors per lane
-  u32x4 kv[NKV], vv[NVV];
-#pragma unroll
-  for (int it = 0; it < NKV; ++it)
-    kv[it] = lane < len ? *reinterpret_cast<const u32x4 *>(kbase + (size_t)lane * qk_row + wave * (DK / 4) + it * V)
-                        : u32x4{0, 0, 0, 0};
-#pragma unroll
-  for (int it = 0; it < NVV; ++it)
-    vv[it] = lane < len ? *reinterpret_cast<const u32x4 *>(vbase + (size_t)lane * v_row + wave * (DV / 4) + it * V)
-                        : u32x4{0, 0, 0, 0};
-  // this lane's queries in accumulator layout (channels 16m + 4grp .. +3), for Q'
-  f32x4 qacc[KT];
-#pragma unroll
-  for (int m = 0; m < KT; ++m) qacc[m] = rq < len ? load4(qbase + (size_t)rq * qk_row + 16 * m + 4 * grp) : zero4();
-  const float bval = (tid < kChunk && tid < len) ? a.beta[(size_t)(start + tid) * a.Hv + h] : 0.f;
-  constexpr int GPT = KDA ? kChunk * DK / kLocalThreads : 1;  // KDA: gate values per thread
-  float gk[GPT];
-  if constexpr (KDA) {
-    // thread = (channel d, token segment): GPT consecutive tokens of one channel
-    const int d = tid % DK, seg = tid / DK;
-    const float *gb = a.g + ((size_t)start * a.Hv + h) * DK + d;
-#pragma unroll
-    for (int u = 0; u < GPT; ++u) {
-      const int r = seg * GPT + u;
-      gk[u] = r < len ? gb[(size_t)r * a.Hv * DK] : 0.f;
-    }
-  } else {
-    gk[0] = (tid < kChunk && tid < len) ? a.g[(size_t)(start + tid) * a.Hv + h] : 0.f;
-  }
+  constexpr int NKV = In::NKV, NVV = In::NVV, GPT = In::GPT;
+  const u32x4(&kv)[NKV] = in.kv;
+  const u32x4(&vv)[NVV] = in.vv;
+  const Frag<T>(&qf)[DK / 32] = in.qf;
+  const f32x4(&qacc)[KT] = in.qacc;
+  float(&gk)[GPT] = in.gk;
+  const float bval = in.bval;
 
   // ---- stage K (token rows and channel rows) and V (channel rows); the
   //      channel-row writes of one wave cover 64 consecutive tokens of one row
@@ -181,6 +252,9 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
     for (int u = 0; u < GPT; ++u) sGam[(seg * GPT + u) * L::LDG + d] = gk[u] + off;
   }
   __syncthreads();
+  // keys, values, gates and betas of this item are staged: the next item's
+  // load now, behind this item's products
+  if (kKvgAhead && nxt.len > 0) in.load_kvg(a, nxt);
 
   // ---- op #2, transposed: wave i owns tokens r in [16i, 16i+16) as the
   //      columns of A^T and P^T and computes the row blocks s = 16j.. (j <= i).
@@ -489,20 +563,51 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       store4(ol_out + ((size_t)m * 64 + lane) * 16 + 4 * wave, acc);
     }
   }
+  if (!local_persistent<T, KDA>() || nxt.len <= 0) break;  // uniform: chunk-major items
+  if constexpr (kQAhead) in.load_q(a, nxt);
+  __syncthreads();  // the next item's staging overwrites every LDS region
+  item += gridDim.x;
+  cur = nxt;
+  }  // item loop
+}
+
+// Resident workgroups per device for the persistent grid: CUs x workgroups
+// that fit on one CU (LDS and registers), looked up once per device.
+template <typename T, int DK, int DV, bool KDA>
+static hipError_t resident_groups(int *out) {
+  using L = LocalLayout<T, DK, DV, KDA>;
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cache[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const int slot = dev < kMaxDevices ? dev : kMaxDevices - 1;
+  int n = dev < kMaxDevices ? cache[slot].load(std::memory_order_relaxed) : 0;
+  if (n == 0) {
+    const void *kern = reinterpret_cast<const void *>(&chunk_local_kernel<T, DK, DV, KDA>);
+    if ((e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::bytes)) != hipSuccess)
+      return e;
+    int cus = 0, per_cu = 0;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kLocalThreads, L::bytes)) != hipSuccess)
+      return e;
+    n = (cus > 0 ? cus : 1) * (per_cu > 0 ? per_cu : 1);
+    if (dev < kMaxDevices) cache[slot].store(n, std::memory_order_relaxed);
+  }
+  *out = n;
+  return hipSuccess;
 }
 
 template <typename T, int DK, int DV, bool KDA>
 static hipError_t launch_local_t(const PrefillArgs &a, hipStream_t stream) {
   using L = LocalLayout<T, DK, DV, KDA>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&chunk_local_kernel<T, DK, DV, KDA>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::bytes);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  hipLaunchKernelGGL((chunk_local_kernel<T, DK, DV, KDA>), dim3(a.max_chunks, a.Hv),
-                     dim3(kLocalThreads), L::bytes, stream, a);
+  int groups = 0;
+  hipError_t e = resident_groups<T, DK, DV, KDA>(&groups);  // also sets the LDS attribute
+  if (e != hipSuccess) return e;
+  const long items = (long)a.max_chunks * a.Hv;
+  const long grid = local_persistent<T, KDA>() && items > groups ? groups : items;
+  hipLaunchKernelGGL((chunk_local_kernel<T, DK, DV, KDA>), dim3((unsigned)grid), dim3(kLocalThreads), L::bytes,
+                     stream, a);
   return hipGetLastError();
 }
 
