@@ -61,7 +61,7 @@ def measured_traffic(kernel: str, workload: str):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(inp, budget_s=10.0, max_reps=40):
+def cpu_baseline(inp, budget_s=10.0, max_reps=400):
     import oracle
     threads = max(1, min(16, len(os.sched_getaffinity(0))))
     oracle.build(force=False)
