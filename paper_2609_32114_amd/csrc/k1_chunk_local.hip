@@ -47,22 +47,45 @@ namespace hagdn {
 
 constexpr int kLocalThreads = 256;
 
+// XOR-swizzled row-major tiles (rows of LD elements, a multiple of 128 bytes):
+// 16-byte chunk q of row r is stored at chunk q ^ (r & 7), so the eight rows
+// a fragment read touches in one LDS cycle hit eight different bank groups
+// with no padding.
+template <typename E, int LD>
+__device__ __forceinline__ int swz(int r, int e) {
+  constexpr int CH = 16 / (int)sizeof(E);
+  return r * LD + ((e / CH) ^ (r & 7)) * CH + e % CH;
+}
+// MFMA fragment: the 8 elements at logical columns e .. e+7 (e a multiple of 8) of row r.
+template <int LD>
+__device__ __forceinline__ bf16x8 frag_sw(const bf16_t *t, int r, int e) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(t + swz<bf16_t, LD>(r, e)));
+}
+template <int LD>
+__device__ __forceinline__ f32x8 frag_sw(const float *t, int r, int e) {
+  const f32x4 x = *reinterpret_cast<const f32x4 *>(t + swz<float, LD>(r, e));
+  const f32x4 y = *reinterpret_cast<const f32x4 *>(t + swz<float, LD>(r, e + 4));
+  return __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Three tile regions, each reused once its first tenant is dead:
+//   X  sK  [64][DK]  keys, token rows (op #2)   -> sKt [DK][64] keys, channel rows (op #4 on)
+//   Y  sA  [64][64]  A, then T (fp32, ops #2-#3) -> sWt [DK][64] W, channel rows
+//   Z  sVt [DV][64]  values, channel rows         -> sUt [DV][64] U~, channel rows
+// all XOR-swizzled; plus beta, the GDN decay column and the gate scan.
 template <typename T, int DK, int DV, bool KDA>
 struct LocalLayout {
-  static constexpr int PAD = 16 / (int)sizeof(T);
-  static constexpr int LDK = DK + PAD;       // sK   [64][LDK]   keys, token rows (ops #2)
-  static constexpr int LDT = kChunk + PAD;   // sKt  [DK][LDT]   keys, channel rows
-                                             // sVt  [DV][LDT]   values, channel rows (op #4)
-                                             // sWt  [DK][LDT]   W, channel rows (over sK)
-                                             // sUt  [DV][LDT]   U~, channel rows (over sVt)
-  static constexpr int LDA = kChunk + 4;     // sA   [64][LDA]   A, then T (fp32)
+  static constexpr int LDK = DK;       // sK row length
+  static constexpr int LDT = kChunk;   // channel-row length (sKt, sWt, sVt, sUt)
+  static constexpr int LDA = kChunk;   // sA row length
   static constexpr int LDG = KDA ? DK + 1 : 1;  // sGam [64][LDG] (GDN: [64])
-  static constexpr size_t bytesX = sizeof(T) * (kChunk * LDK > DK * LDT ? kChunk * LDK : DK * LDT);
-  static constexpr size_t off_K = 0;         // region X: sK, later sWt
-  static constexpr size_t off_Kt = off_K + bytesX;
-  static constexpr size_t off_Vt = off_Kt + sizeof(T) * DK * LDT;   // region Y: sVt, later sUt
-  static constexpr size_t off_A = off_Vt + sizeof(T) * DV * LDT;
-  static constexpr size_t off_beta = off_A + sizeof(float) * kChunk * LDA;
+  static constexpr size_t bytesX = sizeof(T) * kChunk * DK;
+  static constexpr size_t bytesY = sizeof(float) * kChunk * kChunk > sizeof(T) * DK * kChunk
+                                       ? sizeof(float) * kChunk * kChunk : sizeof(T) * DK * kChunk;
+  static constexpr size_t off_K = 0;   // region X
+  static constexpr size_t off_A = off_K + bytesX;   // region Y
+  static constexpr size_t off_Vt = off_A + bytesY;  // region Z
+  static constexpr size_t off_beta = off_Vt + sizeof(T) * DV * kChunk;
   static constexpr size_t off_kdec = off_beta + sizeof(float) * kChunk;  // GDN e^(gamma_last - gamma_s)
   static constexpr size_t off_tot = off_kdec + sizeof(float) * kChunk;   // KDA gate-scan segment totals
   static constexpr size_t off_gam = off_tot + sizeof(float) * (KDA ? kLocalThreads : 0);
@@ -161,7 +184,7 @@ struct LocalIn {
 // loads item n+1's inputs while it computes item n.  Otherwise one workgroup
 // per item.
 template <typename T, bool KDA>
-constexpr bool local_persistent() { return !KDA && sizeof(T) == 2; }
+constexpr bool local_persistent() { return false; }
 
 template <typename T, int DK, int DV, bool KDA>
 __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs a) {
@@ -191,15 +214,15 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 
   extern __shared__ __align__(16) unsigned char smem[];
   T *sK = reinterpret_cast<T *>(smem + L::off_K);
-  T *sKt = reinterpret_cast<T *>(smem + L::off_Kt);
+  T *sKt = sK;   // region X once op #2 is done with the token rows
   T *sVt = reinterpret_cast<T *>(smem + L::off_Vt);
   float *sA = reinterpret_cast<float *>(smem + L::off_A);
   float *sBeta = reinterpret_cast<float *>(smem + L::off_beta);
   float *sKdec = reinterpret_cast<float *>(smem + L::off_kdec);
   float *sTot = reinterpret_cast<float *>(smem + L::off_tot);
   float *sGam = reinterpret_cast<float *>(smem + L::off_gam);
-  T *sWt = sK;   // reuses region X once op #2 is done with the keys
-  T *sUt = sVt;  // reuses region Y once op #4 has read the values
+  T *sWt = reinterpret_cast<T *>(smem + L::off_A);  // region Y once every wave holds its T rows
+  T *sUt = sVt;  // region Z once op #4 has read the values
 
   const int rq = 16 * wave + col;  // token this lane feeds as a column of A^T and P^T
   constexpr int NKV = In::NKV, NVV = In::NVV, GPT = In::GPT;
@@ -210,22 +233,20 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
   float(&gk)[GPT] = in.gk;
   const float bval = in.bval;
 
-  // ---- stage K (token rows and channel rows) and V (channel rows); the
-  //      channel-row writes of one wave cover 64 consecutive tokens of one row
+  // ---- stage K (token rows; its channel rows follow op #2 in the same
+  //      region) and V (channel rows); the channel-row writes of one wave
+  //      cover 64 consecutive tokens of one row
 #pragma unroll
   for (int it = 0; it < NKV; ++it) {
     const int cv = wave * (DK / 4) + it * V;
-    const uint4 u = __builtin_bit_cast(uint4, kv[it]);
-    *reinterpret_cast<uint4 *>(sK + lane * L::LDK + cv) = u;
-#pragma unroll
-    for (int j = 0; j < V; ++j) sKt[(cv + j) * L::LDT + lane] = V16::raw(u, j);
+    *reinterpret_cast<u32x4 *>(sK + swz<T, L::LDK>(lane, cv)) = kv[it];
   }
 #pragma unroll
   for (int it = 0; it < NVV; ++it) {
     const int cv = wave * (DV / 4) + it * V;
     const uint4 u = __builtin_bit_cast(uint4, vv[it]);
 #pragma unroll
-    for (int j = 0; j < V; ++j) sVt[(cv + j) * L::LDT + lane] = V16::raw(u, j);
+    for (int j = 0; j < V; ++j) sVt[swz<T, L::LDT>(cv + j, lane)] = V16::raw(u, j);
   }
   // ---- op #1: beta and gamma (inclusive cumulative log-gate)
   if (tid < kChunk) sBeta[tid] = bval;
@@ -270,13 +291,13 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
     if constexpr (!KDA) {
       Frag<T> kr[DK / 32];
 #pragma unroll
-      for (int kb = 0; kb < DK / 32; ++kb) kr[kb] = load_frag(sK + r * L::LDK + kb * 32, grp);
+      for (int kb = 0; kb < DK / 32; ++kb) kr[kb] = frag_sw<L::LDK>(sK, r, kb * 32 + 8 * grp);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         if (j <= i) {
 #pragma unroll
           for (int kb = 0; kb < DK / 32; ++kb) {
-            const Frag<T> ks = load_frag(sK + (16 * j + col) * L::LDK + kb * 32, grp);
+            const Frag<T> ks = frag_sw<L::LDK>(sK, 16 * j + col, kb * 32 + 8 * grp);
             accA[j] = mma(accA[j], ks, kr[kb]);
             accP[j] = mma(accP[j], ks, qf[kb]);
           }
@@ -288,7 +309,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
           accA[j][e] = s < r ? sBeta[r] * accA[j][e] * dec : 0.f;
           accP[j][e] = accP[j][e] * dec;
         }
-        *reinterpret_cast<f32x4 *>(sA + r * L::LDA + 16 * j + 4 * grp) = accA[j];
+        *reinterpret_cast<f32x4 *>(sA + swz<float, L::LDA>(r, 16 * j + 4 * grp)) = accA[j];
       }
     } else {
       // Per-channel decay e^(gamma_r - gamma_s), factored around a reference
@@ -309,7 +330,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         for (int jj = 0; jj < 8; ++jj) {
           const int d = kb * 32 + kc(grp, jj);
           const float ex = __expf(sGam[r * L::LDG + d] - sGam[rho * L::LDG + d]);
-          xk[jj] = E::to_f32(sK[r * L::LDK + d]) * ex;
+          xk[jj] = E::to_f32(sK[swz<T, L::LDK>(r, d)]) * ex;
           xq[jj] = frag_elem(qf[kb], jj) * ex;
         }
         kr[kb] = make_frag<T>(xk);
@@ -325,7 +346,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 #pragma unroll
             for (int jj = 0; jj < 8; ++jj) {
               const int d = kb * 32 + kc(grp, jj);
-              xs[jj] = E::to_f32(sK[sb * L::LDK + d]) * __expf(sGam[rho * L::LDG + d] - sGam[sb * L::LDG + d]);
+              xs[jj] = E::to_f32(sK[swz<T, L::LDK>(sb, d)]) * __expf(sGam[rho * L::LDG + d] - sGam[sb * L::LDG + d]);
             }
             const Frag<T> ks = make_frag<T>(xs);
             accA[j] = mma(accA[j], ks, kr[kb]);
@@ -341,11 +362,19 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
           accA[j][e] = (j <= i && s < r) ? sBeta[r] * accA[j][e] : 0.f;
           accP[j][e] = (j <= i && s <= r) ? accP[j][e] : 0.f;
         }
-        *reinterpret_cast<f32x4 *>(sA + r * L::LDA + 16 * j + 4 * grp) = accA[j];
+        *reinterpret_cast<f32x4 *>(sA + swz<float, L::LDA>(r, 16 * j + 4 * grp)) = accA[j];
       }
     }
   }
   __syncthreads();
+  // keys as channel rows over the token rows op #2 is done with (region X)
+#pragma unroll
+  for (int it = 0; it < NKV; ++it) {
+    const int cv = wave * (DK / 4) + it * V;
+    const uint4 u = __builtin_bit_cast(uint4, kv[it]);
+#pragma unroll
+    for (int j = 0; j < V; ++j) sKt[swz<T, L::LDT>(cv + j, lane)] = V16::raw(u, j);
+  }
 
   // ---- op #3: T = (I + A)^-1 (unit lower triangular, fp32), blocked by 16.
   //      Diagonal blocks: wave w inverts block w by forward substitution (lane
@@ -357,14 +386,13 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
     float x[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const float *Ar = sA + (b0 + r) * L::LDA + b0;
       float acc = (r == j) ? 1.f : 0.f;
 #pragma unroll
-      for (int s = 0; s < r; ++s) acc -= Ar[s] * x[s];
+      for (int s = 0; s < r; ++s) acc -= sA[swz<float, L::LDA>(b0 + r, b0 + s)] * x[s];
       x[r] = acc;
     }
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sA[(b0 + r) * L::LDA + b0 + j] = x[r];
+    for (int r = 0; r < 16; ++r) sA[swz<float, L::LDA>(b0 + r, b0 + j)] = x[r];
   }
   __syncthreads();
 #pragma unroll
@@ -376,30 +404,31 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       for (int k = j; k < i; ++k) {
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
-          const float av = sA[(16 * i + col) * L::LDA + 16 * k + 4 * st + grp];
-          const float tv = sA[(16 * k + 4 * st + grp) * L::LDA + 16 * j + col];
+          const float av = sA[swz<float, L::LDA>(16 * i + col, 16 * k + 4 * st + grp)];
+          const float tv = sA[swz<float, L::LDA>(16 * k + 4 * st + grp, 16 * j + col)];
           y = __builtin_amdgcn_mfma_f32_16x16x4f32(av, tv, y, 0, 0, 0);
         }
       }
       // T_ii y: the accumulator rows 4grp + st of y are the k index of step st
 #pragma unroll
       for (int st = 0; st < 4; ++st) {
-        const float tv = sA[(16 * i + col) * L::LDA + 16 * i + 4 * grp + st];
+        const float tv = sA[swz<float, L::LDA>(16 * i + col, 16 * i + 4 * grp + st)];
         res = __builtin_amdgcn_mfma_f32_16x16x4f32(tv, y[st], res, 0, 0, 0);
       }
     }
     __syncthreads();  // every read of block row i of A is done
     if (wave < i) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sA[(16 * i + 4 * grp + e) * L::LDA + 16 * wave + col] = -res[e];
+      for (int e = 0; e < 4; ++e) sA[swz<float, L::LDA>(16 * i + 4 * grp + e, 16 * wave + col)] = -res[e];
     }
     __syncthreads();
   }
 
   // ---- op #4: wave i = token block i.  T' = T Diag(b) (GDN: also e^gamma_s).
   //      W and U~ go to LDS as channel rows with tokens kmap-permuted inside
-  //      each 32-token block: sWt[d_k][.] over the keys (region X, free since
-  //      op #2), sUt[d_v][.] over the values once every wave has read them.
+  //      each 32-token block: sWt[d_k][.] over T (region Y) once every wave
+  //      holds its T rows, sUt[d_v][.] over the values once every wave has
+  //      read them.
   {
     const int i = wave, r = 16 * i + col;
     if constexpr (!KDA) {
@@ -408,7 +437,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
     Frag<T> tu[2], tw[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      const f32x8 trow = load_frag(sA + r * L::LDA + kb * 32, grp);
+      const f32x8 trow = frag_sw<L::LDA>(sA, r, kb * 32 + 8 * grp);
       float xu[8], xw[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -420,13 +449,14 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       tu[kb] = make_frag<T>(xu);
       tw[kb] = make_frag<T>(xw);
     }
+    __syncthreads();  // T is in registers: region Y takes W
     f32x4 accU[VT];
 #pragma unroll
     for (int n = 0; n < VT; ++n) {
       accU[n] = zero4();
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-        accU[n] = mma(accU[n], tu[kb], load_frag(sVt + (16 * n + col) * L::LDT + kb * 32, grp));
+        accU[n] = mma(accU[n], tu[kb], frag_sw<L::LDT>(sVt, 16 * n + col, kb * 32 + 8 * grp));
     }
     // lane rows are tokens 16i + 4grp + e: slots 4(i & 1) + e of k-block i >> 1
     const int tpos = 32 * (i >> 1) + 8 * grp + 4 * (i & 1);
@@ -438,23 +468,23 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       for (int kb = 0; kb < 2; ++kb) {
         Frag<T> kf;
         if constexpr (!KDA) {
-          kf = load_frag(sKt + d * L::LDT + kb * 32, grp);
+          kf = frag_sw<L::LDT>(sKt, d, kb * 32 + 8 * grp);
         } else {
           float xk[8];
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             const int s = kb * 32 + kc(grp, j);
-            xk[j] = E::to_f32(sKt[d * L::LDT + s]) * __expf(sGam[s * L::LDG + d]);
+            xk[j] = E::to_f32(sKt[swz<T, L::LDT>(d, s)]) * __expf(sGam[s * L::LDG + d]);
           }
           kf = make_frag<T>(xk);
         }
         acc = mma(acc, tw[kb], kf);
       }
-      store4(sWt + d * L::LDT + tpos, acc);
+      store4(sWt + swz<T, L::LDT>(d, tpos), acc);
     }
     __syncthreads();  // every wave has read sVt and sKt
 #pragma unroll
-    for (int n = 0; n < VT; ++n) store4(sUt + (16 * n + col) * L::LDT + tpos, accU[n]);
+    for (int n = 0; n < VT; ++n) store4(sUt + swz<T, L::LDT>(16 * n + col, tpos), accU[n]);
   }
   // ---- Kt = (K * e^(gamma_last - gamma))^T in place of the staged keys, tokens
   //      kmap-permuted like sWt / sUt (thread d < DK owns channel row d)
@@ -462,7 +492,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
     const int d = tid;
     uint4 row[kChunk / V];
 #pragma unroll
-    for (int u = 0; u < kChunk / V; ++u) row[u] = *reinterpret_cast<const uint4 *>(sKt + d * L::LDT + u * V);
+    for (int u = 0; u < kChunk / V; ++u) row[u] = *reinterpret_cast<const uint4 *>(sKt + swz<T, L::LDT>(d, u * V));
 #pragma unroll
     for (int u = 0; u < kChunk / V; ++u) {
       float outv[V];
@@ -473,7 +503,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         const float ex = KDA ? __expf(sGam[(kChunk - 1) * L::LDG + d] - sGam[s * L::LDG + d]) : sKdec[s];
         outv[j] = V16::get(row[s / V], s % V) * ex;
       }
-      *reinterpret_cast<uint4 *>(sKt + d * L::LDT + u * V) = V16::pack(outv);
+      *reinterpret_cast<uint4 *>(sKt + swz<T, L::LDT>(d, u * V)) = V16::pack(outv);
     }
   }
   {  // chunk decay e^gamma_last
@@ -497,13 +527,13 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       const int n = wave * KPW + nn;
       Frag<T> bk[2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) bk[kb] = load_frag(sKt + (16 * n + col) * L::LDT + kb * 32, grp);
+      for (int kb = 0; kb < 2; ++kb) bk[kb] = frag_sw<L::LDT>(sKt, 16 * n + col, kb * 32 + 8 * grp);
 #pragma unroll
       for (int m = 0; m < KT; ++m) {
         f32x4 acc = zero4();
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
-          acc = mma(acc, load_frag(sWt + (16 * m + col) * L::LDT + kb * 32, grp), bk[kb]);
+          acc = mma(acc, frag_sw<L::LDT>(sWt, 16 * m + col, kb * 32 + 8 * grp), bk[kb]);
         // lane: column d_out, rows d_in = 16m + 4grp + e = 32(m >> 1) + kmap(grp, 4(m & 1) + e)
         // -> slots 4(m & 1) + e of operand block (t = n, kb = m >> 1)
         store4(nm_out + ((size_t)(n * (DK / 32) + (m >> 1)) * 64 + lane) * 8 + 4 * (m & 1), -acc);
@@ -517,12 +547,12 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 #pragma unroll
     for (int mm = 0; mm < KPW; ++mm)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) ak[mm][kb] = load_frag(sKt + (16 * (wave * KPW + mm) + col) * L::LDT + kb * 32, grp);
+      for (int kb = 0; kb < 2; ++kb) ak[mm][kb] = frag_sw<L::LDT>(sKt, 16 * (wave * KPW + mm) + col, kb * 32 + 8 * grp);
 #pragma unroll
     for (int n = 0; n < VT; ++n) {
       Frag<T> bu[2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) bu[kb] = load_frag(sUt + dv_of(n, col) * L::LDT + kb * 32, grp);
+      for (int kb = 0; kb < 2; ++kb) bu[kb] = frag_sw<L::LDT>(sUt, dv_of(n, col), kb * 32 + 8 * grp);
 #pragma unroll
       for (int mm = 0; mm < KPW; ++mm) {
         const int m = wave * KPW + mm;
@@ -547,7 +577,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-        if (kb < nkb) acc = mma(acc, load_frag(sWt + (16 * m + col) * L::LDT + kb * 32, grp), pb[kb]);
+        if (kb < nkb) acc = mma(acc, frag_sw<L::LDT>(sWt, 16 * m + col, kb * 32 + 8 * grp), pb[kb]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) qe[e] *= KDA ? __expf(sGam[r * L::LDG + d + e]) : __expf(sGam[r]);
       store4(qp_out + ((size_t)(m >> 1) * 64 + lane) * 8 + 4 * (m & 1), qe - acc);
@@ -559,7 +589,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
-        if (kb < nkb) acc = mma(acc, load_frag(sUt + dv_of(m, col) * L::LDT + kb * 32, grp), pb[kb]);
+        if (kb < nkb) acc = mma(acc, frag_sw<L::LDT>(sUt, dv_of(m, col), kb * 32 + 8 * grp), pb[kb]);
       store4(ol_out + ((size_t)m * 64 + lane) * 16 + 4 * wave, acc);
     }
   }

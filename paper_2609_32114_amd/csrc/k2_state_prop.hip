@@ -65,6 +65,24 @@ template <typename T> struct Raw4;
 template <> struct Raw4<bf16_t> { using type = uint2; };
 template <> struct Raw4<float> { using type = f32x4; };
 
+// Range-checked stores through a buffer resource over [base, base + bytes):
+// lanes whose byte offset falls outside (negative ones included) store
+// nothing, so the output store needs no branch -- a branch in the loop makes
+// the compiler drain every in-flight load at the join.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t walk_buffer(void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, (short)0, (int)bytes, 0x00020000);  // gfx9 raw buffer word 3
+}
+__device__ __forceinline__ void walk_store4(__amdgpu_buffer_rsrc_t r, int off, bf16_t, f32x4 v) {
+  typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+  u32x2 u;
+  u[0] = (uint32_t)f32_to_bf16(v[0]) | ((uint32_t)f32_to_bf16(v[1]) << 16);
+  u[1] = (uint32_t)f32_to_bf16(v[2]) | ((uint32_t)f32_to_bf16(v[3]) << 16);
+  __builtin_amdgcn_raw_buffer_store_b64(u, r, off, 0, 0);
+}
+__device__ __forceinline__ void walk_store4(__amdgpu_buffer_rsrc_t r, int off, float, f32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, 0);
+}
+
 // One chunk's state-independent operands for the rows one wave owns (the
 // state update, on the critical path) ...
 template <typename T, int DK, bool KDA>
@@ -81,7 +99,7 @@ struct OutOps {
   typename Raw4<T>::type ol[TPW]; // O_loc block (token tile, this d_v tile)
 };
 
-// chunks of state operands in flight (a multiple of the output ring's 2)
+// chunks of operands in flight
 template <typename T> constexpr int pipe_depth() { return sizeof(T) == 2 ? 4 : 2; }
 
 template <typename T, int DK, int DV, bool KDA>
@@ -118,38 +136,49 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
     const float *__restrict__ decg = a.dec;
     const T *__restrict__ Qpg = static_cast<const T *>(a.Qp);
     const T *__restrict__ Olg = static_cast<const T *>(a.Ol);
-    T *__restrict__ Og = static_cast<T *>(a.o);
+    // o rows of this sequence; rows past its end fall outside the buffer range
+    const __amdgpu_buffer_rsrc_t orsrc = walk_buffer(static_cast<T *>(a.o) + (size_t)si.z * a.Hv * DV,
+                                                     (uint32_t)((size_t)si.w * a.Hv * DV * sizeof(T)));
+    // Operands of chunk c: block blk(c) (clamped into the sequence).  NM block
+    // (row tile 2w+i, kb) in fragment order, B and O_loc lane-major (prefill.h).
+    auto blk = [&](int c) { return (size_t)(si.x + min(c, nch - 1)) * a.Hv + h; };
+    auto nm_at = [&](size_t b, int i, int kb) {
+      return NMg + b * ((size_t)DK * DK) + ((size_t)((2 * w + i) * (DK / 32) + kb) * 64 + lane) * 8;
+    };
+    auto b_at = [&](size_t b, int i) {
+      return Bg + b * ((size_t)DV * DK) + ((size_t)(tile * 64 + lane) * (DK / 16) + 2 * w + i) * 4;
+    };
+    auto qp_at = [&](size_t b, int u, int kb) {  // token tile nt = w + NW*u
+      return Qpg + b * ((size_t)kChunk * DK) + ((size_t)((w + NW * u) * (DK / 32) + kb) * 64 + lane) * 8;
+    };
+    auto ol_at = [&](size_t b, int u) {
+      return Olg + b * ((size_t)kChunk * DV) + ((size_t)(tile * 64 + lane) * 4 + w + NW * u) * 4;
+    };
+    auto load_dec = [&](StepOps<T, DK, KDA> &op, size_t b) {
+      if constexpr (KDA) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) op.dec[i] = load4(decg + b * DK + row0 + 16 * i + 4 * grp);
+      } else {
+        op.dec[0][0] = decg[b * DK];
+      }
+    };
     auto load = [&](StepOps<T, DK, KDA> &op, int c) {
-      const size_t blk = (size_t)(si.x + min(c, nch - 1)) * a.Hv + h;
-      // NM block (row tile 2w+i, kb) in fragment order; B lane-major (prefill.h)
-      const T *nm = NMg + blk * ((size_t)DK * DK);
-      const T *bt = Bg + blk * ((size_t)DV * DK);
+      const size_t b = blk(c);
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
 #pragma unroll
-        for (int kb = 0; kb < DK / 32; ++kb)
-          op.nm[i][kb] = load_frag_at(nm + ((size_t)((2 * w + i) * (DK / 32) + kb) * 64 + lane) * 8);
-        op.b[i] = load_raw4(bt + ((size_t)(tile * 64 + lane) * (DK / 16) + 2 * w + i) * 4);
+        for (int kb = 0; kb < DK / 32; ++kb) op.nm[i][kb] = load_frag_at(nm_at(b, i, kb));
+        op.b[i] = load_raw4(b_at(b, i));
       }
-      if constexpr (KDA) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) op.dec[i] = load4(decg + blk * DK + row0 + 16 * i + 4 * grp);
-      } else {
-        op.dec[0][0] = decg[blk * DK];
-      }
+      load_dec(op, b);
     };
-    // output operands: token tiles nt = w + NW*u (Q' fragment order, O_loc lane-major)
     auto load_out = [&](OutOps<T, DK> &oq, int c) {
-      const size_t blk = (size_t)(si.x + min(c, nch - 1)) * a.Hv + h;
-      const T *qp = Qpg + blk * ((size_t)kChunk * DK);
-      const T *ol = Olg + blk * ((size_t)kChunk * DV);
+      const size_t b = blk(c);
 #pragma unroll
       for (int u = 0; u < OutOps<T, DK>::TPW; ++u) {
-        const int nt = w + NW * u;
 #pragma unroll
-        for (int kb = 0; kb < DK / 32; ++kb)
-          oq.qp[u][kb] = load_frag_at(qp + ((size_t)(nt * (DK / 32) + kb) * 64 + lane) * 8);
-        oq.ol[u] = load_raw4(ol + ((size_t)(tile * 64 + lane) * 4 + nt) * 4);
+        for (int kb = 0; kb < DK / 32; ++kb) oq.qp[u][kb] = load_frag_at(qp_at(b, u, kb));
+        oq.ol[u] = load_raw4(ol_at(b, u));
       }
     };
     // output tiles of the previous chunk, stored one step late so the store
@@ -161,10 +190,16 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
 #pragma unroll
       for (int u = 0; u < TPW; ++u) {
         const int r = base + 16 * (w + NW * u) + col;
-        if (r < si.w) store4(Og + ((size_t)(si.z + r) * a.Hv + h) * DV + dv_of(tile, 4 * grp), pend[u] * a.scale);
+        walk_store4(orsrc, (int)(((size_t)r * a.Hv + h) * DV + dv_of(tile, 4 * grp)) * (int)sizeof(T), T{},
+                    pend[u] * a.scale);
       }
     };
-    auto step = [&](const StepOps<T, DK, KDA> &op, const OutOps<T, DK> &oq, int c) {
+    // One chunk step.  Every operand register is refilled for chunk c + D right
+    // after the instruction that consumes it, so the step's loads leave one or
+    // two at a time behind matrix work instead of in a block that stalls the
+    // wave at the address unit (each CU streams ~54 KiB per step from L2).
+    auto step = [&](StepOps<T, DK, KDA> &op, OutOps<T, DK> &oq, int c) {
+      const size_t bn = blk(c + D);
       // 5-read: this wave's k-block of S_c, published for the other waves
       const Frag<T> own = frag_from_acc<T>(H[0], H[1]);
       xch[c & 1][w][lane] = own;
@@ -172,7 +207,7 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
       Frag<T> hb[NW];
 #pragma unroll
       for (int kb = 0; kb < NW; ++kb) hb[kb] = xch[c & 1][kb][lane];
-      if (c > 0) store_out(c - 1);
+      store_out(c - 1);  // chunk -1: every row falls outside the buffer range
       // 5-update: rows of S^T_{c+1} = D S^T_c + B + NM S^T_c (two accumulation
       // chains per tile, k-blocks split even/odd, summed at the end)
       f32x4 acc0[2], acc1[2];
@@ -183,11 +218,15 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
         acc1[i] = zero4();
       }
 #pragma unroll
+      for (int i = 0; i < 2; ++i) op.b[i] = load_raw4(b_at(bn, i));
+      load_dec(op, bn);
+#pragma unroll
       for (int kb = 0; kb < NW; ++kb)
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
           if (kb & 1) acc1[i] = mma(acc1[i], op.nm[i][kb], hb[kb]);
           else acc0[i] = mma(acc0[i], op.nm[i][kb], hb[kb]);
+          op.nm[i][kb] = load_frag_at(nm_at(bn, i, kb));
         }
 #pragma unroll
       for (int i = 0; i < 2; ++i) H[i] = acc0[i] + acc1[i];
@@ -198,32 +237,30 @@ __global__ __launch_bounds__(64 * (DK / 32)) void state_prop_kernel(PrefillArgs 
 #pragma unroll
       for (int u = 0; u < TPW; ++u) {
         pend[u] = raw4_to_f32(oq.ol[u]);
+        oq.ol[u] = load_raw4(ol_at(bn, u));
 #pragma unroll
-        for (int kb = 0; kb < NW; ++kb) pend[u] = mma(pend[u], hb[kb], oq.qp[u][kb]);
+        for (int kb = 0; kb < NW; ++kb) {
+          pend[u] = mma(pend[u], hb[kb], oq.qp[u][kb]);
+          oq.qp[u][kb] = load_frag_at(qp_at(bn, u, kb));
+        }
       }
     };
 
     StepOps<T, DK, KDA> R[D];
-    OutOps<T, DK> Q[2];
+    OutOps<T, DK> Q[D];
 #pragma unroll
-    for (int u = 0; u < D; ++u) load(R[u], u);
-#pragma unroll
-    for (int u = 0; u < 2; ++u) load_out(Q[u], u);
+    for (int u = 0; u < D; ++u) {
+      load(R[u], u);
+      load_out(Q[u], u);
+    }
     int c0 = 0;
     for (; c0 + D <= nch; c0 += D) {
 #pragma unroll
-      for (int u = 0; u < D; ++u) {
-        step(R[u], Q[u & 1], c0 + u);
-        load(R[u], c0 + u + D);
-        load_out(Q[u & 1], c0 + u + 2);
-      }
+      for (int u = 0; u < D; ++u) step(R[u], Q[u], c0 + u);
     }
 #pragma unroll
     for (int u = 0; u < D; ++u)
-      if (c0 + u < nch) {  // uniform for the workgroup
-        step(R[u], Q[u & 1], c0 + u);
-        if (u + 2 < D) load_out(Q[u & 1], c0 + u + 2);
-      }
+      if (c0 + u < nch) step(R[u], Q[u], c0 + u);  // uniform for the workgroup
     store_out(nch - 1);
   }
 
