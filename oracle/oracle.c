@@ -187,3 +187,52 @@ int oracle_kda_prefill(const double *q, const double *k, const double *v,
   return oracle_run(1, q, k, v, g, beta, s0, cu_seqlens, N, T_total, Hqk, Hv,
                     Dk, Dv, scale, o, s_final, nthreads);
 }
+
+/*
+ * Preprocessing of raw projections, the step in front of the recurrence.
+ * The paper accelerates the layer's projections around the LA core by
+ * operator fusion (Sec. 7, "Implementation and Evaluation", full-layer
+ * implementation); the elementwise maps that turn projections into the
+ * recurrence's inputs are the ones its workloads use (per-token L2
+ * normalisation of q and k, a softplus log-gate and a sigmoid write strength).
+ * In place, fp64, one token at a time:
+ *
+ *   flag 1  q_t <- q_t / max(||q_t||_2, 1e-6) and the same for k_t, per token
+ *           and query/key head
+ *   flag 2  g <- -softplus(g) = -log(1 + e^g), every element (GDN [T, Hv],
+ *           KDA [T, Hv, Dk])
+ *   flag 4  beta <- 1 / (1 + e^-beta)
+ *
+ * softplus is evaluated as max(x, 0) + log1p(e^-|x|), which is log(1 + e^x)
+ * rearranged so that the exponential never overflows.
+ * Returns 0, or -1 on an invalid argument (nothing changed).
+ */
+int oracle_preprocess(double *q, double *k, double *g, double *beta, int T,
+                      int Hqk, int Hv, int Dk, int kda, int flags) {
+  if (T < 0 || Hqk < 1 || Hv < 1 || Dk < 1 || (flags & ~7)) return -1;
+  if (T == 0) return 0;
+  if (!q || !k || !g || !beta) return -1;
+  if (flags & 1) {
+    for (size_t r = 0; r < (size_t)T * Hqk; ++r) {
+      double *rows[2] = {q + r * Dk, k + r * Dk};
+      for (int w = 0; w < 2; ++w) {
+        double ss = 0.0;
+        for (int i = 0; i < Dk; ++i) ss += rows[w][i] * rows[w][i];
+        double nrm = sqrt(ss);
+        if (nrm < 1e-6) nrm = 1e-6;
+        for (int i = 0; i < Dk; ++i) rows[w][i] /= nrm;
+      }
+    }
+  }
+  if (flags & 2) {
+    const size_t n = (size_t)T * Hv * (kda ? Dk : 1);
+    for (size_t e = 0; e < n; ++e) {
+      const double x = g[e];
+      g[e] = -((x > 0.0 ? x : 0.0) + log1p(exp(-fabs(x))));
+    }
+  }
+  if (flags & 4) {
+    for (size_t e = 0; e < (size_t)T * Hv; ++e) beta[e] = 1.0 / (1.0 + exp(-beta[e]));
+  }
+  return 0;
+}
