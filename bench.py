@@ -2,7 +2,7 @@
 """Throughput of GDN prefill on one MI355X: tokens/s, roofline fraction, CPU oracle beside it.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload 1] [--no-cpu-baseline]
-                    [--segment-chunks L]
+                    [--segment-chunks L] [--pre] [--decode]
 
 One step = one full gdn_prefill call (chunk index, chunk-local, segment maps,
 state propagation with output) over the workload: by default one sequence of 4096
@@ -14,6 +14,12 @@ from cache.  The timed region holds only the K steps; per-kernel times come
 from HIP events the library records on the launch stream around each kernel
 during a second pass over the same K steps (events inside the timed region
 would add their own GPU time, about 3 us each, to every step).
+
+--pre times the same prefill from raw projections with every in-kernel
+preprocessing flag (q/k L2 normalisation, softplus gate, sigmoid beta).
+--decode times the decode step instead: one token for each of 256 sequences
+(H = 16, d = 128, bf16, fp32 state pool updated in place); its metric is
+decode tokens/s.
 
 Prints ONE JSON line.
 """
@@ -31,6 +37,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "GDN prefill tokens/s at H=16,d=128,T=4096 bf16; % of HBM/MFMA roofline"
+DECODE_METRIC = "GDN decode tokens/s (one token per sequence, 256 sequences) at H=16,d=128 bf16"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
@@ -41,7 +48,8 @@ def kernel_source_hash(name: str) -> str:
     csrc = os.path.join(ROOT, "paper_2609_32114_amd", "csrc")
     files = {"chunk_local": ("k1_chunk_local.hip",),
              "state_prop": ("k2_state_prop.hip", "k3_segments.hip"),
-             "seg_transfer": ("k3_segments.hip",), "chunk_index": ("k0_chunk_index.hip",)}
+             "seg_transfer": ("k3_segments.hip",), "chunk_index": ("k0_chunk_index.hip",),
+             "decode": ("k4_decode.hip",)}
     h = hashlib.sha256()
     for f in files[name] + ("device.h", "prefill.h"):
         with open(os.path.join(csrc, f), "rb") as fh:
@@ -61,13 +69,13 @@ def measured_traffic(kernel: str, workload: str):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(inp, budget_s=10.0, max_reps=400):
+def cpu_baseline(inp, budget_s=10.0, max_reps=400, pre=0):
     import oracle
     threads = max(1, min(16, len(os.sched_getaffinity(0))))
     oracle.build(force=False)
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.run_inputs(inp, nthreads=threads)
+        oracle.run_inputs(inp, nthreads=threads, pre=pre)
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s or reps >= max_reps:
@@ -88,6 +96,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--segment-chunks", type=int, default=0,
                     help="segment length of the state chain in 64-token chunks (0: automatic)")
+    ap.add_argument("--pre", action="store_true",
+                    help="prefill from raw projections with every in-kernel preprocessing flag")
+    ap.add_argument("--decode", action="store_true", help="time the decode step instead of prefill")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (10 times): the known-size "
                          "reference that scales rocprofv3 FETCH_SIZE / WRITE_SIZE counts")
@@ -108,6 +119,9 @@ def main():
               "run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
+    if args.decode:
+        return bench_decode(args)
+
     import numpy as np
     import torch
 
@@ -118,7 +132,8 @@ def main():
     P.load_library()
     P.set_segment_chunks(args.segment_chunks)
     wl = WORKLOADS[args.workload]
-    inp = make_workload(args.workload)
+    pre = P.PRE_ALL if args.pre else 0
+    inp = make_workload(args.workload, raw=bool(pre))
     kda = inp.kind == "kda"
     dev = "cuda:0"
     torch.cuda.set_device(0)
@@ -144,7 +159,7 @@ def main():
     def step(i):
         c = copies[i % len(copies)]
         fn(c["q"], c["k"], c["v"], c["g"], c["beta"], initial_state=c["s0"], cu_seqlens=cu,
-           scale=inp.scale, workspace=ws, out=o, final_out=sf)
+           scale=inp.scale, workspace=ws, out=o, final_out=sf, preprocess=pre)
 
     for i in range(args.warmup):
         step(i)
@@ -175,7 +190,8 @@ def main():
                                   seg_chunks=L)
     dom_ms = kernel_ms[dom]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    traffic = measured_traffic(dom, wl.name)
+    wname = wl.name + (f"_pre{pre}" if pre else "")
+    traffic = measured_traffic(dom, wname)
     path_bytes = cost.algorithmic_bytes(T, N, Hqk, Hv, Dk, Dv, esz, kda, inp.s0 is not None)
     path_flops = cost.flops(T, Hv, 64, Dk, Dv)
     out = {
@@ -191,9 +207,10 @@ def main():
         "vs_baseline": None,
         "dtype": inp.dtype,
         "data": "synthetic",
-        "config": {"workload": wl.name, "kind": inp.kind, "sequences": N, "seq_len": T,
+        "config": {"workload": wname, "kind": inp.kind, "sequences": N, "seq_len": T,
                    "q_k_heads": Hqk, "v_heads": Hv, "head_dim_k": Dk, "head_dim_v": Dv,
-                   "chunk": 64, "segment_chunks": L, "input_copies": len(copies)},
+                   "chunk": 64, "segment_chunks": L, "input_copies": len(copies),
+                   "preprocess": pre},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "bytes_per_launch": dom_bytes, "kernel_ms": dom_ms},
@@ -206,7 +223,84 @@ def main():
         "kernel_calls_timed": ncalls,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(inp)
+        out["cpu_baseline"] = cpu_baseline(inp, pre=pre)
+    print(json.dumps(out), flush=True)
+
+
+def bench_decode(args):
+    """Decode step: K steps over the 256-sequence batch, then a profiled pass."""
+    import numpy as np
+    import torch
+
+    import paper_2609_32114_amd as P
+    from paper_2609_32114_amd import cost
+    from paper_2609_32114_amd.inputs import DECODE_WORKLOAD as W, make_decode_case
+
+    P.load_library()
+    torch.cuda.set_device(0)
+    dev = "cuda:0"
+    di = make_decode_case(kind=W["kind"], N=W["N"], Hqk=W["Hqk"], Hv=W["Hv"], Dk=W["Dk"],
+                          Dv=W["Dv"], dtype=W["dtype"], seed=5)
+    N, Hqk, Hv, Dk, Dv = W["N"], W["Hqk"], W["Hv"], W["Dk"], W["Dv"]
+    dt = torch.bfloat16 if di.dtype == "bf16" else torch.float32
+    esz = 2 if di.dtype == "bf16" else 4
+    t = lambda x, d=torch.float32: torch.from_numpy(np.ascontiguousarray(x)).to(dev).to(d)
+    toks = dict(q=t(di.q, dt), k=t(di.k, dt), v=t(di.v, dt), g=t(di.g), beta=t(di.beta))
+    # two state pools (2 x 256 MiB, more than the 256 MB Infinity Cache) in turn
+    pools = [t(di.state) for _ in range(2)]
+    o = torch.empty((N, Hv, Dv), dtype=dt, device=dev)
+
+    def step(i):
+        P.gdn_decode(toks["q"], toks["k"], toks["v"], toks["g"], toks["beta"], pools[i % 2],
+                     scale=di.scale, out=o)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(args.steps):
+        step(args.warmup + i)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    P.profile_begin(args.steps)
+    for i in range(args.steps):
+        step(args.warmup + i)
+    kernel_ms, ncalls = P.profile_end()
+    kms = kernel_ms["decode"]
+    nbytes = cost.decode_bytes(N, Hqk, Hv, Dk, Dv, esz, False)
+    achieved = nbytes / (kms * 1e-3) / 1e9
+    out = {
+        "metric": DECODE_METRIC, "value": N / (ms * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": di.dtype, "data": "synthetic",
+        "config": {"workload": f"decode_N{N}_H{Hv}_d{Dk}_{di.dtype}", "kind": "gdn",
+                   "sequences": N, "q_k_heads": Hqk, "v_heads": Hv, "head_dim_k": Dk,
+                   "head_dim_v": Dv, "state_pools": len(pools)},
+        "roofline": {"bound": "hbm", "kernel": "decode", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic("decode", f"decode_N{N}_H{Hv}_d{Dk}_{di.dtype}"),
+                     "bytes_per_launch": nbytes, "kernel_ms": kms},
+        "kernels_ms": {"decode": kms},
+        "kernel_calls_timed": ncalls,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = max(1, min(16, len(os.sched_getaffinity(0))))
+        oracle.build(force=False)
+        reps, t0 = 0, time.perf_counter()
+        while True:
+            oracle.decode("gdn", di.q, di.k, di.v, di.g, di.beta, di.state, di.scale,
+                          nthreads=threads)
+            reps += 1
+            el = time.perf_counter() - t0
+            if el >= 10.0 or reps >= 400:
+                break
+        out["cpu_baseline"] = {"value": reps * N / el, "unit": "tokens/s", "cores": threads,
+                               "kind": "oracle",
+                               "sample": f"the full decode batch ({N} sequences x {Hv} heads) "
+                                         f"repeated {reps}x, {el:.1f} s, fp64"}
     print(json.dumps(out), flush=True)
 
 

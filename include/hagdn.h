@@ -112,6 +112,70 @@ int kda_prefill(const void *q, const void *k, const void *v, const float *g,
                 float scale, int dtype, void *o, float *s_final,
                 void *workspace, size_t workspace_bytes, void *stream);
 
+/* Preprocessing flags (bit mask) for gdn_prefill_ex, kda_prefill_ex and the
+ * decode entry points.  They fold the elementwise maps that turn a layer's raw
+ * projections into the recurrence's inputs into the kernels' loads, so the
+ * caller makes no separate pass over q, k, g and beta (the paper fuses the
+ * layer's projection-side work around the LA core, Sec. 7 "Implementation
+ * and Evaluation", full-layer implementation).  Each flag changes what the
+ * corresponding argument holds:
+ *   HAGDN_PRE_QK_L2NORM      q and k are raw: every token's q and k vector (per
+ *                            q/k head) is divided by max(||x||_2, 1e-6) in fp32
+ *                            before use (bf16: the result is rounded to bf16
+ *                            where it is an MFMA operand);
+ *   HAGDN_PRE_GATE_SOFTPLUS  g holds raw values x; the log-gate is -softplus(x)
+ *                            = -log(1 + e^x), computed in fp32;
+ *   HAGDN_PRE_BETA_SIGMOID   beta holds raw values x; the write strength is
+ *                            1 / (1 + e^-x), computed in fp32.
+ * Any other bit is rejected with HAGDN_EINVAL. */
+typedef enum {
+  HAGDN_PRE_QK_L2NORM = 1,
+  HAGDN_PRE_GATE_SOFTPLUS = 2,
+  HAGDN_PRE_BETA_SIGMOID = 4
+} hagdn_pre_flags;
+
+/* gdn_prefill / kda_prefill with preprocessing flags `pre` (a mask of
+ * hagdn_pre_flags; 0 gives exactly gdn_prefill / kda_prefill).  Same
+ * workspace size as without flags. */
+int gdn_prefill_ex(const void *q, const void *k, const void *v, const float *g,
+                   const float *beta, const float *s0, const int32_t *cu_seqlens,
+                   int N, int T_total, int Hqk, int Hv, int Dk, int Dv,
+                   float scale, int dtype, int pre, void *o, float *s_final,
+                   void *workspace, size_t workspace_bytes, void *stream);
+int kda_prefill_ex(const void *q, const void *k, const void *v, const float *g,
+                   const float *beta, const float *s0, const int32_t *cu_seqlens,
+                   int N, int T_total, int Hqk, int Hv, int Dk, int Dv,
+                   float scale, int dtype, int pre, void *o, float *s_final,
+                   void *workspace, size_t workspace_bytes, void *stream);
+
+/* One decode step: a single new token for each of N sequences, advanced by
+ * the token-by-token recurrence (paper Sec. 2.1, which notes that the
+ * recurrent form serves decoding; Sec. 7.3 leaves decode to the serving
+ * backend).  Starting from the state a prefill left in s_final, repeated
+ * calls continue the sequence exactly as a longer prefill would (up to
+ * rounding).
+ *   q, k   [N, Hqk, Dk] dtype        v, o  [N, Hv, Dv] dtype
+ *   g      GDN [N, Hv] / KDA [N, Hv, Dk] fp32 log-gate     beta [N, Hv] fp32
+ *   state  [num_slots, Hv, Dk, Dv] fp32, a pool of states in the s_final
+ *          layout, read and UPDATED IN PLACE
+ *   slots  [N] int32 DEVICE memory, or NULL: sequence n uses pool slot
+ *          slots[n] (NULL: slot n, and num_slots is taken as N).  A slot
+ *          outside [0, num_slots) marks a padding entry: its output row is
+ *          written as zeros and no state is touched.  Two live entries must
+ *          not name the same slot (their updates would race).
+ *   pre    preprocessing flags (hagdn_pre_flags).
+ * No workspace.  N = 0 is a no-op.  Alignment: q, k, v, o and state
+ * 16-byte aligned; g, beta, slots 4-byte aligned.  Returns a hagdn_status;
+ * on a non-OK return nothing was launched (except HAGDN_EHIP). */
+int gdn_decode(const void *q, const void *k, const void *v, const float *g,
+               const float *beta, float *state, const int32_t *slots,
+               int num_slots, int N, int Hqk, int Hv, int Dk, int Dv,
+               float scale, int dtype, int pre, void *o, void *stream);
+int kda_decode(const void *q, const void *k, const void *v, const float *g,
+               const float *beta, float *state, const int32_t *slots,
+               int num_slots, int N, int Hqk, int Hv, int Dk, int Dv,
+               float scale, int dtype, int pre, void *o, void *stream);
+
 /* Message for the last non-OK return on this host thread ("" if none). */
 const char *hagdn_last_error(void);
 
@@ -122,12 +186,13 @@ int hagdn_device_status(const void *workspace, size_t workspace_bytes,
                         void *stream, int *code);
 
 /* Per-kernel timing with HIP events recorded on the call's stream around each
- * kernel of every gdn_prefill / kda_prefill call made on this host thread
- * between begin and end (at most max_calls calls are recorded; later calls run
+ * kernel of every prefill and decode call made on this host thread between
+ * begin and end (at most max_calls calls are recorded; later calls run
  * untimed).  hagdn_profile_end synchronises the recorded events and writes,
- * for each kernel i < min(max_kernels, hagdn_kernel_count()), the mean
- * duration in milliseconds into mean_ms[i]; *calls receives the number of
- * calls timed.  Returns a hagdn_status. */
+ * for each kernel i < min(max_kernels, hagdn_kernel_count()), its mean
+ * duration in milliseconds over the calls that launched it into mean_ms[i]
+ * (0 if none did); *calls receives the number of calls timed.  Returns a
+ * hagdn_status. */
 int hagdn_profile_begin(int max_calls);
 int hagdn_profile_end(double *mean_ms, int max_kernels, int *calls);
 int hagdn_kernel_count(void);

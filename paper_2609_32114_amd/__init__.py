@@ -8,13 +8,17 @@ step of the computation runs in the library's HIP kernels; there is no CPU or
 PyTorch fallback, and calls fail loudly when the library is missing.
 
     o, s_final = gdn_prefill(q, k, v, g, beta, initial_state=None,
-                             cu_seqlens=None, scale=1.0)
+                             cu_seqlens=None, scale=1.0, preprocess=0)
+    o = gdn_decode(q1, k1, v1, g1, beta1, state_pool, slots=None, scale=1.0)
 
 Layouts: q, k [T, Hqk, Dk]; v [T, Hv, Dv] (bf16 or fp32, all the same dtype);
 g [T, Hv] fp32 (KDA: [T, Hv, Dk]); beta [T, Hv] fp32; initial_state
 [N, Hv, Dk, Dv] fp32; cu_seqlens int32 [N+1] on the device (None: one
 sequence of length T).  Returns o [T, Hv, Dv] in the input dtype and the final
-state [N, Hv, Dk, Dv] fp32.
+state [N, Hv, Dk, Dv] fp32.  ``preprocess`` (PRE_* flags) makes the kernels
+normalise raw q/k and map raw gate / beta projections as they load them.
+The decode entry points advance one token per sequence and update a state
+pool in place.
 """
 
 from __future__ import annotations
@@ -22,8 +26,8 @@ from __future__ import annotations
 import ctypes
 import os
 
-__all__ = ["gdn_prefill", "kda_prefill", "workspace_size", "device_status", "library_path",
-           "load_library", "profile_begin", "profile_end", "kernel_names", "set_segment_chunks",
+__all__ = ["gdn_prefill", "kda_prefill", "gdn_decode", "kda_decode", "workspace_size",
+           "device_status", "library_path", "load_library", "profile_begin", "profile_end", "kernel_names", "set_segment_chunks",
            "segment_chunks", "HagdnError"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -32,17 +36,25 @@ _lib = None
 
 HAGDN_F32, HAGDN_BF16 = 0, 1
 DEV_OK, DEV_BAD_SEQLENS = 0, 1
+# preprocessing flags (hagdn_pre_flags)
+PRE_QK_L2NORM, PRE_GATE_SOFTPLUS, PRE_BETA_SIGMOID = 1, 2, 4
+PRE_ALL = 7
+
+_PREFILL_ARGS = ([ctypes.c_void_p] * 7 + [ctypes.c_int] * 6 + [ctypes.c_float, ctypes.c_int])
+_PREFILL_TAIL = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+_DECODE_ARGS = ([ctypes.c_void_p] * 7 + [ctypes.c_int] * 6 +
+                [ctypes.c_float, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p])
 
 _SYMBOLS = {
     # name: (restype, argtypes)
     "gdn_prefill_workspace_size": (ctypes.c_size_t, [ctypes.c_int] * 7),
     "kda_prefill_workspace_size": (ctypes.c_size_t, [ctypes.c_int] * 7),
-    "gdn_prefill": (ctypes.c_int, [ctypes.c_void_p] * 7 + [ctypes.c_int] * 6 +
-                    [ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
-                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
-    "kda_prefill": (ctypes.c_int, [ctypes.c_void_p] * 7 + [ctypes.c_int] * 6 +
-                    [ctypes.c_float, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
-                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "gdn_prefill": (ctypes.c_int, _PREFILL_ARGS + _PREFILL_TAIL),
+    "kda_prefill": (ctypes.c_int, _PREFILL_ARGS + _PREFILL_TAIL),
+    "gdn_prefill_ex": (ctypes.c_int, _PREFILL_ARGS + [ctypes.c_int] + _PREFILL_TAIL),
+    "kda_prefill_ex": (ctypes.c_int, _PREFILL_ARGS + [ctypes.c_int] + _PREFILL_TAIL),
+    "gdn_decode": (ctypes.c_int, _DECODE_ARGS),
+    "kda_decode": (ctypes.c_int, _DECODE_ARGS),
     "hagdn_last_error": (ctypes.c_char_p, []),
     "hagdn_device_status": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                                            ctypes.POINTER(ctypes.c_int)]),
@@ -113,7 +125,7 @@ def _ptr(t):
 
 
 def _prefill(kind, q, k, v, g, beta, initial_state, cu_seqlens, scale, output_final_state,
-             workspace, out, final_out):
+             workspace, out, final_out, preprocess=0):
     import torch
     lib = load_library()
     if not (q.is_cuda and k.is_cuda and v.is_cuda and g.is_cuda and beta.is_cuda):
@@ -152,27 +164,79 @@ def _prefill(kind, q, k, v, g, beta, initial_state, cu_seqlens, scale, output_fi
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev).cuda_stream
-    fn = lib.gdn_prefill if kind == "gdn" else lib.kda_prefill
+    fn = lib.gdn_prefill_ex if kind == "gdn" else lib.kda_prefill_ex
     rc = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(initial_state), _ptr(cu_seqlens),
-            N, T, Hqk, Hv, Dk, Dv, float(scale), dt, _ptr(o), _ptr(sf), _ptr(workspace),
-            workspace.numel() * workspace.element_size(), ctypes.c_void_p(stream))
+            N, T, Hqk, Hv, Dk, Dv, float(scale), dt, int(preprocess), _ptr(o), _ptr(sf),
+            _ptr(workspace), workspace.numel() * workspace.element_size(), ctypes.c_void_p(stream))
     if rc != 0:
         raise HagdnError(rc, _err(lib))
     return o, sf
 
 
 def gdn_prefill(q, k, v, g, beta, initial_state=None, cu_seqlens=None, scale=1.0,
-                output_final_state=True, workspace=None, out=None, final_out=None):
-    """Gated DeltaNet prefill.  Returns (o, final_state or None)."""
+                output_final_state=True, workspace=None, out=None, final_out=None, preprocess=0):
+    """Gated DeltaNet prefill.  Returns (o, final_state or None).
+
+    preprocess: a mask of PRE_* flags; q, k, g and beta then hold raw
+    projections that the kernels normalise / map as they load them."""
     return _prefill("gdn", q, k, v, g, beta, initial_state, cu_seqlens, scale, output_final_state,
-                    workspace, out, final_out)
+                    workspace, out, final_out, preprocess)
 
 
 def kda_prefill(q, k, v, g, beta, initial_state=None, cu_seqlens=None, scale=1.0,
-                output_final_state=True, workspace=None, out=None, final_out=None):
+                output_final_state=True, workspace=None, out=None, final_out=None, preprocess=0):
     """KDA prefill (per-key-channel log-gate g [T, Hv, Dk]).  Returns (o, final_state or None)."""
     return _prefill("kda", q, k, v, g, beta, initial_state, cu_seqlens, scale, output_final_state,
-                    workspace, out, final_out)
+                    workspace, out, final_out, preprocess)
+
+
+def _decode(kind, q, k, v, g, beta, state, slots, scale, preprocess, out):
+    import torch
+    lib = load_library()
+    for name, t in (("q", q), ("k", k), ("v", v), ("g", g), ("beta", beta), ("state", state)):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous GPU tensor")
+    if not (q.dtype == k.dtype == v.dtype):
+        raise TypeError("q, k, v must share one dtype")
+    dt = _dtype_code(q.dtype)
+    if g.dtype != torch.float32 or beta.dtype != torch.float32 or state.dtype != torch.float32:
+        raise TypeError("g, beta and state must be float32")
+    N, Hqk, Dk = q.shape
+    Hv, Dv = v.shape[1], v.shape[2]
+    if k.shape != q.shape or v.shape[0] != N:
+        raise ValueError("shape mismatch between q, k, v")
+    gshape = (N, Hv) if kind == "gdn" else (N, Hv, Dk)
+    if tuple(g.shape) != gshape or tuple(beta.shape) != (N, Hv):
+        raise ValueError(f"g must be {gshape} and beta {(N, Hv)}")
+    if state.dim() != 4 or tuple(state.shape[1:]) != (Hv, Dk, Dv):
+        raise ValueError(f"state must be [slots, {Hv}, {Dk}, {Dv}]")
+    if slots is None:
+        if state.shape[0] < N:
+            raise ValueError("without slots the state pool needs one state per sequence")
+    elif slots.dtype != torch.int32 or not slots.is_cuda or tuple(slots.shape) != (N,) \
+            or not slots.is_contiguous():
+        raise TypeError("slots must be a contiguous int32 GPU tensor of length N")
+    o = out if out is not None else torch.empty((N, Hv, Dv), dtype=q.dtype, device=q.device)
+    stream = torch.cuda.current_stream(q.device).cuda_stream
+    fn = lib.gdn_decode if kind == "gdn" else lib.kda_decode
+    rc = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(state), _ptr(slots),
+            int(state.shape[0]), N, Hqk, Hv, Dk, Dv, float(scale), dt, int(preprocess), _ptr(o),
+            ctypes.c_void_p(stream))
+    if rc != 0:
+        raise HagdnError(rc, _err(lib))
+    return o
+
+
+def gdn_decode(q, k, v, g, beta, state, slots=None, scale=1.0, preprocess=0, out=None):
+    """One GDN decode step: q, k [N, Hqk, Dk], v [N, Hv, Dv], g, beta [N, Hv].
+    Updates the fp32 state pool [S, Hv, Dk, Dv] in place (sequence n in slot
+    slots[n], or n) and returns o [N, Hv, Dv]."""
+    return _decode("gdn", q, k, v, g, beta, state, slots, scale, preprocess, out)
+
+
+def kda_decode(q, k, v, g, beta, state, slots=None, scale=1.0, preprocess=0, out=None):
+    """One KDA decode step (g [N, Hv, Dk]); see gdn_decode."""
+    return _decode("kda", q, k, v, g, beta, state, slots, scale, preprocess, out)
 
 
 def device_status(workspace) -> int:

@@ -77,3 +77,19 @@ def kernel_bytes(kernel: str, T_total: int, N: int, Hqk: int, Hv: int, dk: int, 
         wr = T_total * Hv * dv * e + state
         return rd + wr
     raise KeyError(kernel)
+
+
+def decode_bytes(N: int, Hqk: int, Hv: int, dk: int, dv: int, elt_bytes: int, kda: bool,
+                 slots: bool = False) -> int:
+    """Compulsory bytes of one decode step over N live sequences: q, k, v, o of
+    one token each (I/O dtype), gate and beta (fp32), and the fp32 state of
+    every (sequence, value head) read once and written once (plus the slot
+    indices when given)."""
+    e = elt_bytes
+    tok = N * (2 * Hqk * dk * e + 2 * Hv * dv * e + Hv * 4 * (dk if kda else 1) + Hv * 4)
+    return tok + 2 * N * Hv * dk * dv * 4 + (4 * N if slots else 0)
+
+
+def decode_flops(N: int, Hv: int, dk: int, dv: int) -> float:
+    """Decay, H^T k, rank-1 update and H^T q: about 4 multiply-adds per state element."""
+    return 8.0 * N * Hv * dk * dv

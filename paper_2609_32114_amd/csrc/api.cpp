@@ -12,7 +12,9 @@
 //   or, when every sequence is one segment,
 //   K3 state prop     (N x Hv x Dv/16 workgroups)          operator #5 per chain, fused
 //                                                          with operator #6
-// No allocation, no synchronisation, no pointer retained after return.
+// The decode entry points enqueue one kernel (k4_decode.hip) and use no
+// workspace.  No allocation, no synchronisation, no pointer retained after
+// return.
 #include <hip/hip_runtime.h>
 
 #include <stdarg.h>
@@ -42,8 +44,10 @@ int fail(int code, const char *fmt, ...) {
 }
 
 constexpr size_t kAlign = 256;
-constexpr int kNumKernels = 4;
-const char *const kKernelNames[kNumKernels] = {"chunk_index", "chunk_local", "seg_transfer", "state_prop"};
+constexpr int kNumKernels = 5;
+const char *const kKernelNames[kNumKernels] = {"chunk_index", "chunk_local", "seg_transfer", "state_prop",
+                                               "decode"};
+constexpr int kDecodeKernel = 4;
 
 // Chunks per segment of the state chain; 0 = chosen per call (seg_chunks).
 std::atomic<int> g_seg_override{0};
@@ -164,10 +168,11 @@ void prof_release() {
 
 int prefill(bool kda, const void *q, const void *k, const void *v, const float *g,
             const float *beta, const float *s0, const int32_t *cu, int N, int T, int Hqk, int Hv,
-            int Dk, int Dv, float scale, int dtype, void *o, float *s_final, void *ws,
+            int Dk, int Dv, float scale, int dtype, int pre, void *o, float *s_final, void *ws,
             size_t ws_bytes, void *stream_) {
   int rc = check_shapes(N, T, Hqk, Hv, Dk, Dv, dtype);
   if (rc != HAGDN_OK) return rc;
+  if (pre & ~hagdn::kPreAll) return fail(HAGDN_EINVAL, "unknown preprocessing flags 0x%x", pre);
   if (!cu || !ws) return fail(HAGDN_EINVAL, "NULL required pointer (cu_seqlens, workspace)");
   // token tensors are never dereferenced for an empty batch (torch hands out
   // NULL for zero-size allocations)
@@ -196,6 +201,7 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   a.N = N; a.T = T; a.Hqk = Hqk; a.Hv = Hv; a.Dk = Dk; a.Dv = Dv;
   a.max_chunks = L.max_chunks;
   a.scale = scale;
+  a.pre = pre;
   a.o = o; a.s_final = s_final;
   a.status = reinterpret_cast<int *>(w + L.status);
   a.seq_info = reinterpret_cast<int4 *>(w + L.seq_info);
@@ -245,6 +251,44 @@ hip_fail:
   return fail(HAGDN_EHIP, "HIP error: %s", hipGetErrorString(e));
 }
 
+int decode(bool kda, const void *q, const void *k, const void *v, const float *g,
+           const float *beta, float *state, const int32_t *slots, int num_slots, int N, int Hqk,
+           int Hv, int Dk, int Dv, float scale, int dtype, int pre, void *o, void *stream) {
+  if (N < 0) return fail(HAGDN_EINVAL, "N must be >= 0 (got %d)", N);
+  int rc = check_shapes(N > 0 ? N : 1, 0, Hqk, Hv, Dk, Dv, dtype);
+  if (rc != HAGDN_OK) return rc;
+  if (pre & ~hagdn::kPreAll) return fail(HAGDN_EINVAL, "unknown preprocessing flags 0x%x", pre);
+  if (N == 0) return HAGDN_OK;
+  if (!slots) num_slots = N;
+  if (num_slots < 1) return fail(HAGDN_EINVAL, "num_slots must be >= 1 (got %d)", num_slots);
+  if ((size_t)N * Hv * (Dv / 32) > 0x7fffffffu) return fail(HAGDN_EINVAL, "N x Hv too large");
+  if (!q || !k || !v || !g || !beta || !state || !o)
+    return fail(HAGDN_EINVAL, "NULL required pointer (q, k, v, g, beta, state, o)");
+  const void *p16[] = {q, k, v, o, state};
+  const char *n16[] = {"q", "k", "v", "o", "state"};
+  for (int i = 0; i < 5; ++i)
+    if (!aligned(p16[i], 16)) return fail(HAGDN_EINVAL, "%s is not 16-byte aligned", n16[i]);
+  if (!aligned(g, 4) || !aligned(beta, 4) || !aligned(slots, 4))
+    return fail(HAGDN_EINVAL, "g, beta and slots must be 4-byte aligned");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipEvent_t *ev = nullptr;
+  if (g_prof.on && g_prof.calls < g_prof.max_calls) {
+    ev = &g_prof.ev[(size_t)g_prof.calls * (kNumKernels + 1)];
+    unsigned char *ran = &g_prof.ran[(size_t)g_prof.calls * kNumKernels];
+    ++g_prof.calls;
+    for (int i = 0; i < kNumKernels; ++i) ran[i] = i == kDecodeKernel;
+  }
+  hagdn::DecodeArgs a;
+  a.q = q; a.k = k; a.v = v; a.g = g; a.beta = beta; a.state = state; a.slots = slots;
+  a.N = N; a.Hqk = Hqk; a.Hv = Hv; a.Dk = Dk; a.Dv = Dv; a.num_slots = num_slots;
+  a.scale = scale; a.pre = pre; a.o = o;
+  hipError_t e = ev ? hipEventRecord(ev[0], st) : hipSuccess;
+  if (e == hipSuccess) e = hagdn::launch_decode(a, dtype == HAGDN_BF16, kda, st);
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[kDecodeKernel + 1], st);
+  if (e != hipSuccess) return fail(HAGDN_EHIP, "HIP error: %s", hipGetErrorString(e));
+  return HAGDN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -262,7 +306,37 @@ int gdn_prefill(const void *q, const void *k, const void *v, const float *g, con
                 int Dk, int Dv, float scale, int dtype, void *o, float *s_final, void *workspace,
                 size_t workspace_bytes, void *stream) {
   return prefill(false, q, k, v, g, beta, s0, cu_seqlens, N, T_total, Hqk, Hv, Dk, Dv, scale,
-                 dtype, o, s_final, workspace, workspace_bytes, stream);
+                 dtype, 0, o, s_final, workspace, workspace_bytes, stream);
+}
+
+int gdn_prefill_ex(const void *q, const void *k, const void *v, const float *g, const float *beta,
+                   const float *s0, const int32_t *cu_seqlens, int N, int T_total, int Hqk, int Hv,
+                   int Dk, int Dv, float scale, int dtype, int pre, void *o, float *s_final,
+                   void *workspace, size_t workspace_bytes, void *stream) {
+  return prefill(false, q, k, v, g, beta, s0, cu_seqlens, N, T_total, Hqk, Hv, Dk, Dv, scale,
+                 dtype, pre, o, s_final, workspace, workspace_bytes, stream);
+}
+
+int kda_prefill_ex(const void *q, const void *k, const void *v, const float *g, const float *beta,
+                   const float *s0, const int32_t *cu_seqlens, int N, int T_total, int Hqk, int Hv,
+                   int Dk, int Dv, float scale, int dtype, int pre, void *o, float *s_final,
+                   void *workspace, size_t workspace_bytes, void *stream) {
+  return prefill(true, q, k, v, g, beta, s0, cu_seqlens, N, T_total, Hqk, Hv, Dk, Dv, scale,
+                 dtype, pre, o, s_final, workspace, workspace_bytes, stream);
+}
+
+int gdn_decode(const void *q, const void *k, const void *v, const float *g, const float *beta,
+               float *state, const int32_t *slots, int num_slots, int N, int Hqk, int Hv, int Dk,
+               int Dv, float scale, int dtype, int pre, void *o, void *stream) {
+  return decode(false, q, k, v, g, beta, state, slots, num_slots, N, Hqk, Hv, Dk, Dv, scale, dtype,
+                pre, o, stream);
+}
+
+int kda_decode(const void *q, const void *k, const void *v, const float *g, const float *beta,
+               float *state, const int32_t *slots, int num_slots, int N, int Hqk, int Hv, int Dk,
+               int Dv, float scale, int dtype, int pre, void *o, void *stream) {
+  return decode(true, q, k, v, g, beta, state, slots, num_slots, N, Hqk, Hv, Dk, Dv, scale, dtype,
+                pre, o, stream);
 }
 
 int kda_prefill(const void *q, const void *k, const void *v, const float *g, const float *beta,
@@ -270,7 +344,7 @@ int kda_prefill(const void *q, const void *k, const void *v, const float *g, con
                 int Dk, int Dv, float scale, int dtype, void *o, float *s_final, void *workspace,
                 size_t workspace_bytes, void *stream) {
   return prefill(true, q, k, v, g, beta, s0, cu_seqlens, N, T_total, Hqk, Hv, Dk, Dv, scale,
-                 dtype, o, s_final, workspace, workspace_bytes, stream);
+                 dtype, 0, o, s_final, workspace, workspace_bytes, stream);
 }
 
 const char *hagdn_last_error(void) { return g_err.c_str(); }
@@ -309,16 +383,21 @@ int hagdn_profile_end(double *mean_ms, int max_kernels, int *calls) {
   if (!g_prof.on) return fail(HAGDN_EINVAL, "profiling was not started");
   const int nc = g_prof.calls;
   std::vector<double> sum(kNumKernels, 0.0);
+  std::vector<int> runs(kNumKernels, 0);
   for (int c = 0; c < nc; ++c) {
     hipEvent_t *ev = &g_prof.ev[(size_t)c * (kNumKernels + 1)];
     const unsigned char *ran = &g_prof.ran[(size_t)c * kNumKernels];
-    hipError_t r = hipEventSynchronize(ev[kNumKernels]);
+    int last = -1;  // the call's last kernel: its end event is the call's last event
+    for (int i = 0; i < kNumKernels; ++i)
+      if (ran[i]) last = i;
+    hipError_t r = last >= 0 ? hipEventSynchronize(ev[last + 1]) : hipSuccess;
     hipEvent_t prev = ev[0];
     for (int i = 0; i < kNumKernels && r == hipSuccess; ++i) {
-      if (!ran[i]) continue;  // not launched in this call: 0 ms
+      if (!ran[i]) continue;  // not launched in this call
       float ms = 0.f;
       r = hipEventElapsedTime(&ms, prev, ev[i + 1]);
       sum[i] += ms;
+      ++runs[i];
       prev = ev[i + 1];
     }
     if (r != hipSuccess) {
@@ -327,7 +406,7 @@ int hagdn_profile_end(double *mean_ms, int max_kernels, int *calls) {
     }
   }
   for (int i = 0; i < kNumKernels && i < max_kernels && mean_ms; ++i)
-    mean_ms[i] = nc ? sum[i] / nc : 0.0;
+    mean_ms[i] = runs[i] ? sum[i] / runs[i] : 0.0;
   if (calls) *calls = nc;
   prof_release();
   return HAGDN_OK;

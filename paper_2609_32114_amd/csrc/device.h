@@ -233,6 +233,23 @@ __device__ __forceinline__ f32x4 mma(f32x4 acc, f32x8 a, f32x8 b) {
   return acc;
 }
 
+// ------------------------------------------------ input preprocessing maps
+// Raw projection -> log-gate: -softplus(x) = -(max(x, 0) + log(1 + e^-|x|)),
+// the form in which the exponential cannot overflow.
+__device__ __forceinline__ float neg_softplus(float x) {
+  return -(fmaxf(x, 0.f) + log1pf(expf(-fabsf(x))));
+}
+// Raw projection -> write strength in (0, 1).
+__device__ __forceinline__ float sigmoid(float x) { return 1.f / (1.f + expf(-x)); }
+// Factor that L2-normalises a vector with squared norm ss (norm floored at 1e-6).
+__device__ __forceinline__ float inv_l2(float ss) { return 1.f / fmaxf(sqrtf(ss), 1e-6f); }
+// Sum over the 64 lanes of a wave, every lane receives it.
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
 __device__ __forceinline__ f32x4 zero4() {
   f32x4 z = {0.f, 0.f, 0.f, 0.f};
   return z;

@@ -111,7 +111,7 @@ __device__ __forceinline__ LocalItem local_item(const PrefillArgs &a, int item) 
 // Global inputs of one item, loaded one item ahead (padded tokens: zeros).
 // Every load is issued unconditionally from a row clamped into the chunk and
 // the padding is selected away afterwards, so the memory counters stay exact.
-template <typename T, int DK, int DV, bool KDA>
+template <typename T, int DK, int DV, bool KDA, bool PRE>
 struct LocalIn {
   static constexpr int V = 16 / (int)sizeof(T);
   static constexpr int NKV = DK / 4 / V, NVV = DV / 4 / V;       // 16-byte vectors per lane
@@ -142,7 +142,8 @@ struct LocalIn {
     }
     const int rt = min(tid & (kChunk - 1), last);
     const float b = a.beta[(size_t)(it.start + rt) * a.Hv + it.h];
-    bval = (tid < kChunk && tid < it.len) ? b : 0.f;
+    const float bx = (PRE && (a.pre & kPreBetaSigmoid)) ? sigmoid(b) : b;
+    bval = (tid < kChunk && tid < it.len) ? bx : 0.f;
     if constexpr (KDA) {
       const int d = tid % DK, seg = tid / DK;
       const float *gb = a.g + ((size_t)it.start * a.Hv + it.h) * DK + d;
@@ -150,11 +151,12 @@ struct LocalIn {
       for (int u = 0; u < GPT; ++u) {
         const int r = seg * GPT + u;
         const float x = gb[(size_t)min(r, last) * a.Hv * DK];
-        gk[u] = r < it.len ? x : 0.f;
+        gk[u] = r < it.len ? ((PRE && (a.pre & kPreGateSoftplus)) ? neg_softplus(x) : x) : 0.f;
       }
     } else {
       const float x = a.g[(size_t)(it.start + rt) * a.Hv + it.h];
-      gk[0] = (tid < kChunk && tid < it.len) ? x : 0.f;
+      const float gx = (PRE && (a.pre & kPreGateSoftplus)) ? neg_softplus(x) : x;
+      gk[0] = (tid < kChunk && tid < it.len) ? gx : 0.f;
     }
   }
   __device__ __forceinline__ void load_q(const PrefillArgs &a, const LocalItem &it) {
@@ -176,6 +178,49 @@ struct LocalIn {
       qacc[m] = live ? x : zero4();
     }
   }
+  // L2 normalisation of raw keys and queries.  A key row is spread over the
+  // four waves (channel quarters): their partial sums of squares meet in
+  // `scratch` (256 floats, one barrier) and the keys are rescaled in
+  // registers before they are staged.  A query row lives in the four lane
+  // groups of one column (two lane exchanges); its factor is returned and
+  // applied to the products the queries enter (P and Q * e^gamma), which is
+  // the same as scaling the query rows.
+  __device__ __forceinline__ float l2norm_qk(float *scratch) {
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    using V16 = Vec16<T>;
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < NKV; ++i) {
+      const uint4 u = __builtin_bit_cast(uint4, kv[i]);
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const float x = V16::get(u, j);
+        ss += x * x;
+      }
+    }
+    scratch[wave * 64 + lane] = ss;
+    float qs = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < DK / 32; ++kb)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float x = frag_elem(qf[kb], j);
+        qs += x * x;
+      }
+    qs += __shfl_xor(qs, 16);
+    qs += __shfl_xor(qs, 32);
+    __syncthreads();
+    const float ik = inv_l2(scratch[lane] + scratch[64 + lane] + scratch[128 + lane] + scratch[192 + lane]);
+#pragma unroll
+    for (int i = 0; i < NKV; ++i) {
+      const uint4 u = __builtin_bit_cast(uint4, kv[i]);
+      float x[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) x[j] = V16::get(u, j) * ik;
+      kv[i] = __builtin_bit_cast(u32x4, V16::pack(x));
+    }
+    return inv_l2(qs);
+  }
 };
 
 // Persistent where registers allow two workgroups per CU alongside the
@@ -186,12 +231,14 @@ struct LocalIn {
 template <typename T, bool KDA>
 constexpr bool local_persistent() { return false; }
 
-template <typename T, int DK, int DV, bool KDA>
+// PRE: the call carries preprocessing flags (a separate instance, so that the
+// plain path keeps its register budget).
+template <typename T, int DK, int DV, bool KDA, bool PRE>
 __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs a) {
   using L = LocalLayout<T, DK, DV, KDA>;
   using E = Elt<T>;
   using V16 = Vec16<T>;
-  using In = LocalIn<T, DK, DV, KDA>;
+  using In = LocalIn<T, DK, DV, KDA, PRE>;
   constexpr int V = 16 / (int)sizeof(T);  // elements per 16-byte vector
   constexpr int KT = DK / 16, VT = DV / 16;
   constexpr int KPW = KT / 4;             // d_k tiles per wave in the reduce-side products
@@ -232,6 +279,12 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
   const f32x4(&qacc)[KT] = in.qacc;
   float(&gk)[GPT] = in.gk;
   const float bval = in.bval;
+
+  // raw projections: normalise q and k (region Y is free until op #2)
+  float qscale = 1.f;  // L2 factor of this lane's query row rq (raw queries)
+  if constexpr (PRE) {
+    if (a.pre & kPreQkNorm) qscale = in.l2norm_qk(sA);
+  }
 
   // ---- stage K (token rows; its channel rows follow op #2 in the same
   //      region) and V (channel rows); the channel-row writes of one wave
@@ -307,7 +360,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
           const int s = 16 * j + 4 * grp + e;
           const float dec = s <= r ? __expf(sGam[r] - sGam[s]) : 0.f;
           accA[j][e] = s < r ? sBeta[r] * accA[j][e] * dec : 0.f;
-          accP[j][e] = accP[j][e] * dec;
+          accP[j][e] = accP[j][e] * dec * qscale;
         }
         *reinterpret_cast<f32x4 *>(sA + swz<float, L::LDA>(r, 16 * j + 4 * grp)) = accA[j];
       }
@@ -360,7 +413,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         for (int e = 0; e < 4; ++e) {
           const int s = 16 * j + 4 * grp + e;
           accA[j][e] = (j <= i && s < r) ? sBeta[r] * accA[j][e] : 0.f;
-          accP[j][e] = (j <= i && s <= r) ? accP[j][e] : 0.f;
+          accP[j][e] = (j <= i && s <= r) ? accP[j][e] * qscale : 0.f;
         }
         *reinterpret_cast<f32x4 *>(sA + swz<float, L::LDA>(r, 16 * j + 4 * grp)) = accA[j];
       }
@@ -573,7 +626,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 #pragma unroll
     for (int m = 0; m < KT; ++m) {
       const int d = 16 * m + 4 * grp;
-      f32x4 qe = qacc[m];
+      f32x4 qe = qacc[m] * qscale;
       f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -603,7 +656,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 
 // Resident workgroups per device for the persistent grid: CUs x workgroups
 // that fit on one CU (LDS and registers), looked up once per device.
-template <typename T, int DK, int DV, bool KDA>
+template <typename T, int DK, int DV, bool KDA, bool PRE>
 static hipError_t resident_groups(int *out) {
   using L = LocalLayout<T, DK, DV, KDA>;
   constexpr int kMaxDevices = 64;
@@ -614,7 +667,7 @@ static hipError_t resident_groups(int *out) {
   const int slot = dev < kMaxDevices ? dev : kMaxDevices - 1;
   int n = dev < kMaxDevices ? cache[slot].load(std::memory_order_relaxed) : 0;
   if (n == 0) {
-    const void *kern = reinterpret_cast<const void *>(&chunk_local_kernel<T, DK, DV, KDA>);
+    const void *kern = reinterpret_cast<const void *>(&chunk_local_kernel<T, DK, DV, KDA, PRE>);
     if ((e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::bytes)) != hipSuccess)
       return e;
     int cus = 0, per_cu = 0;
@@ -628,31 +681,36 @@ static hipError_t resident_groups(int *out) {
   return hipSuccess;
 }
 
-template <typename T, int DK, int DV, bool KDA>
+template <typename T, int DK, int DV, bool KDA, bool PRE>
 static hipError_t launch_local_t(const PrefillArgs &a, hipStream_t stream) {
   using L = LocalLayout<T, DK, DV, KDA>;
   int groups = 0;
-  hipError_t e = resident_groups<T, DK, DV, KDA>(&groups);  // also sets the LDS attribute
+  hipError_t e = resident_groups<T, DK, DV, KDA, PRE>(&groups);  // also sets the LDS attribute
   if (e != hipSuccess) return e;
   const long items = (long)a.max_chunks * a.Hv;
   const long grid = local_persistent<T, KDA>() && items > groups ? groups : items;
-  hipLaunchKernelGGL((chunk_local_kernel<T, DK, DV, KDA>), dim3((unsigned)grid), dim3(kLocalThreads), L::bytes,
+  hipLaunchKernelGGL((chunk_local_kernel<T, DK, DV, KDA, PRE>), dim3((unsigned)grid), dim3(kLocalThreads), L::bytes,
                      stream, a);
   return hipGetLastError();
 }
 
-template <typename T, bool KDA>
+template <typename T, bool KDA, bool PRE>
 static hipError_t dispatch_dims(const PrefillArgs &a, hipStream_t s) {
-  if (a.Dk == 64 && a.Dv == 64) return launch_local_t<T, 64, 64, KDA>(a, s);
-  if (a.Dk == 64 && a.Dv == 128) return launch_local_t<T, 64, 128, KDA>(a, s);
-  if (a.Dk == 128 && a.Dv == 64) return launch_local_t<T, 128, 64, KDA>(a, s);
-  return launch_local_t<T, 128, 128, KDA>(a, s);
+  if (a.Dk == 64 && a.Dv == 64) return launch_local_t<T, 64, 64, KDA, PRE>(a, s);
+  if (a.Dk == 64 && a.Dv == 128) return launch_local_t<T, 64, 128, KDA, PRE>(a, s);
+  if (a.Dk == 128 && a.Dv == 64) return launch_local_t<T, 128, 64, KDA, PRE>(a, s);
+  return launch_local_t<T, 128, 128, KDA, PRE>(a, s);
+}
+
+template <typename T, bool KDA>
+static hipError_t dispatch_pre(const PrefillArgs &a, hipStream_t s) {
+  return a.pre ? dispatch_dims<T, KDA, true>(a, s) : dispatch_dims<T, KDA, false>(a, s);
 }
 
 hipError_t launch_chunk_local(const PrefillArgs &a, bool bf16, bool kda, hipStream_t s) {
   if (a.max_chunks == 0) return hipSuccess;
-  if (bf16) return kda ? dispatch_dims<bf16_t, true>(a, s) : dispatch_dims<bf16_t, false>(a, s);
-  return kda ? dispatch_dims<float, true>(a, s) : dispatch_dims<float, false>(a, s);
+  if (bf16) return kda ? dispatch_pre<bf16_t, true>(a, s) : dispatch_pre<bf16_t, false>(a, s);
+  return kda ? dispatch_pre<float, true>(a, s) : dispatch_pre<float, false>(a, s);
 }
 
 }  // namespace hagdn

@@ -10,6 +10,13 @@ namespace hagdn {
 
 constexpr int kChunk = 64;  // chunk length C (paper Sec. 7.1 uses C = 64)
 
+// Preprocessing flags (the ABI's HAGDN_PRE_*): maps applied to the raw
+// projections as the kernels load them.
+constexpr int kPreQkNorm = 1;        // q, k <- x / max(||x||_2, 1e-6) per token and head
+constexpr int kPreGateSoftplus = 2;  // g <- -softplus(g)
+constexpr int kPreBetaSigmoid = 4;   // beta <- sigmoid(beta)
+constexpr int kPreAll = 7;
+
 // Everything one prefill call needs, resolved to device pointers.  The
 // workspace regions are carved by api.cpp; per (chunk, value head) block
 // `blk = chunk * Hv + h` each region holds one fixed-size block.  With
@@ -51,6 +58,7 @@ struct PrefillArgs {
   int N, T, Hqk, Hv, Dk, Dv;
   int max_chunks;  // upper bound on chunks: T / 64 + N
   float scale;
+  int pre;         // preprocessing flags (kPre*)
   void *o;
   float *s_final;
   // workspace
@@ -67,6 +75,21 @@ struct PrefillArgs {
   float *Bseg;
 };
 
+// One decode step: a single token for each of N sequences whose states live
+// in a pool of num_slots states, sequence n in slot slots[n] (slots == NULL:
+// slot n).  A slot outside [0, num_slots) is a padding entry: its output row
+// is written as zeros and no state is touched.
+struct DecodeArgs {
+  const void *q, *k, *v;   // [N, Hqk, Dk], [N, Hqk, Dk], [N, Hv, Dv]
+  const float *g, *beta;   // [N, Hv] (KDA g: [N, Hv, Dk]), [N, Hv]
+  float *state;            // [num_slots, Hv, Dk, Dv], read and updated in place
+  const int32_t *slots;    // [N] or NULL
+  int N, Hqk, Hv, Dk, Dv, num_slots;
+  float scale;
+  int pre;                 // preprocessing flags (kPre*)
+  void *o;                 // [N, Hv, Dv]
+};
+
 // Host-side launchers, one per kernel; each picks the template instance for
 // (dtype, Dk, Dv, gate kind) and enqueues on `stream`.
 hipError_t launch_chunk_index(const PrefillArgs &a, hipStream_t stream);
@@ -76,5 +99,7 @@ hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStrea
 // segment-parallel path: segment maps, then ops #5 + #6 per segment
 hipError_t launch_seg_transfer(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
 hipError_t launch_seg_state(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
+// one decode step (N x Hv x Dv/32 workgroups)
+hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool kda, hipStream_t stream);
 
 }  // namespace hagdn

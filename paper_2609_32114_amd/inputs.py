@@ -28,6 +28,12 @@ e^-52 per 64-token chunk, so inter-chunk propagation and s0 barely matter.
   "ks"   key stress: keys from a random 4-dim subspace per head, beta = 1
   "s0"   lm gates plus a nonzero 0.02*N(0,1) initial state
   "lg"   large gates: g = -softplus(3*N(0,1)) (exercises KDA exponent bounds)
+
+raw=True keeps the same draws as raw projections (q, k unnormalised, g and
+beta untransformed) for the kernels' in-kernel preprocessing.  Decode inputs
+(make_decode_case) draw one token per sequence the same way plus a state
+pool; the decode workload is a 256-sequence serving batch with workload 1's
+head shape.
 """
 
 from __future__ import annotations
@@ -109,8 +115,15 @@ class Inputs:
 
 
 def make_case(kind="gdn", lengths=(256,), Hqk=1, Hv=1, Dk=64, Dv=64, dtype="f32",
-              with_s0=False, variant="base", seed=0, scale=1.0, varlen_draw=None) -> Inputs:
-    """Draw one seeded input set.  ``lengths`` may be None with ``varlen_draw``."""
+              with_s0=False, variant="base", seed=0, scale=1.0, varlen_draw=None,
+              raw=False) -> Inputs:
+    """Draw one seeded input set.  ``lengths`` may be None with ``varlen_draw``.
+
+    raw=True returns the raw projections instead (same draws): q and k not
+    normalised, g and beta the untransformed N(0,1) draws, for the kernels'
+    in-kernel preprocessing (base variant only)."""
+    if raw and variant != "base":
+        raise ValueError("raw projections exist for the base variant only")
     rng = np.random.Generator(np.random.PCG64(seed))
     if lengths is None:
         n, lo, hi = varlen_draw
@@ -135,10 +148,13 @@ def make_case(kind="gdn", lengths=(256,), Hqk=1, Hv=1, Dk=64, Dv=64, dtype="f32"
         basis = rng.standard_normal((Hqk, 4, Dk), dtype=np.float32)
         coef = k[:, :, :4]
         k = np.einsum("thc,hcd->thd", coef, basis).astype(np.float32)
-    q = _l2norm(q)
-    k = _l2norm(k)
+    if not raw:
+        q = _l2norm(q)
+        k = _l2norm(k)
 
-    if variant in ("lm", "s0"):
+    if raw:
+        g = g_raw
+    elif variant in ("lm", "s0"):
         g = (np.float32(-0.01) * _softplus(g_raw)).astype(np.float32)
     elif variant == "dn":
         g = np.zeros(gshape, dtype=np.float32)
@@ -147,6 +163,8 @@ def make_case(kind="gdn", lengths=(256,), Hqk=1, Hv=1, Dk=64, Dv=64, dtype="f32"
     else:
         g = -_softplus(g_raw)
     beta = np.ones((T, Hv), dtype=np.float32) if variant == "ks" else _sigmoid(b_raw)
+    if raw:
+        beta = b_raw
 
     if dtype == "bf16":
         q, k, v = round_to_bf16(q), round_to_bf16(k), round_to_bf16(v)
@@ -154,13 +172,69 @@ def make_case(kind="gdn", lengths=(256,), Hqk=1, Hv=1, Dk=64, Dv=64, dtype="f32"
         raise ValueError(dtype)
     return Inputs(kind=kind, dtype=dtype, q=q, k=k, v=v, g=g.astype(np.float32),
                   beta=beta, s0=s0, cu_seqlens=cu, scale=float(scale),
-                  meta=dict(seed=seed, variant=variant, lengths=lengths))
+                  meta=dict(seed=seed, variant=variant, lengths=lengths, raw=raw))
 
 
 def make_workload(idx: int, variant: str = "base", seed: int | None = None,
-                  kind: str | None = None) -> Inputs:
+                  kind: str | None = None, raw: bool = False) -> Inputs:
     w = WORKLOADS[idx]
     return make_case(kind=kind or w.kind, lengths=w.lengths, Hqk=w.Hqk, Hv=w.Hv, Dk=w.Dk,
                      Dv=w.Dv, dtype=w.dtype, with_s0=w.with_s0, variant=variant,
                      seed=1000 + idx if seed is None else seed,
-                     varlen_draw=w.varlen_draw or None)
+                     varlen_draw=w.varlen_draw or None, raw=raw)
+
+
+@dataclass
+class DecodeInputs:
+    kind: str
+    dtype: str
+    q: np.ndarray        # [N, Hqk, Dk]
+    k: np.ndarray
+    v: np.ndarray        # [N, Hv, Dv]
+    g: np.ndarray        # [N, Hv] or [N, Hv, Dk]
+    beta: np.ndarray     # [N, Hv]
+    state: np.ndarray    # [S, Hv, Dk, Dv] fp32 pool
+    slots: np.ndarray | None  # int32 [N] or None
+    scale: float = 1.0
+    meta: dict = field(default_factory=dict)
+
+
+# Decode workload: one token for each of 256 sequences of a serving batch,
+# with the prefill workload's head shape (H = 16, d = 128, bf16).
+DECODE_WORKLOAD = dict(kind="gdn", N=256, Hqk=16, Hv=16, Dk=128, Dv=128, dtype="bf16")
+
+
+def make_decode_case(kind="gdn", N=4, Hqk=1, Hv=1, Dk=64, Dv=64, dtype="f32", pool=None,
+                     pad=0, seed=0, scale=1.0, raw=False) -> DecodeInputs:
+    """One decode step's inputs: a token per sequence drawn like the prefill
+    inputs, a state pool of ``pool`` slots (default N) of 0.1*N(0,1) values (a
+    state a prefill left), and, when pool is given, a random slot per
+    sequence (distinct) with ``pad`` entries set to -1 (padding)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    q = rng.standard_normal((N, Hqk, Dk), dtype=np.float32)
+    k = rng.standard_normal((N, Hqk, Dk), dtype=np.float32)
+    v = rng.standard_normal((N, Hv, Dv), dtype=np.float32)
+    gshape = (N, Hv) if kind == "gdn" else (N, Hv, Dk)
+    g_raw = rng.standard_normal(gshape, dtype=np.float32)
+    b_raw = rng.standard_normal((N, Hv), dtype=np.float32)
+    S = N if pool is None else int(pool)
+    state = np.float32(0.1) * rng.standard_normal((S, Hv, Dk, Dv), dtype=np.float32)
+    slots = None
+    if pool is not None:
+        if S < N - pad:
+            raise ValueError("pool too small for the live sequences")
+        slots = rng.permutation(S)[:N].astype(np.int32)
+        if pad:
+            slots[rng.choice(N, size=pad, replace=False)] = -1
+    if raw:
+        g, beta = g_raw, b_raw
+    else:
+        q, k = _l2norm(q), _l2norm(k)
+        g, beta = -_softplus(g_raw), _sigmoid(b_raw)
+    if dtype == "bf16":
+        q, k, v = round_to_bf16(q), round_to_bf16(k), round_to_bf16(v)
+    elif dtype != "f32":
+        raise ValueError(dtype)
+    return DecodeInputs(kind=kind, dtype=dtype, q=q, k=k, v=v, g=g.astype(np.float32),
+                        beta=beta.astype(np.float32), state=state, slots=slots,
+                        scale=float(scale), meta=dict(seed=seed, N=N, pool=S, pad=pad, raw=raw))

@@ -125,3 +125,52 @@ def test_segment_length_knob():
     finally:
         P.set_segment_chunks(0)
     assert P.segment_chunks(1, 4096, 16, 128) == 64
+
+
+def _call_ex(lib, kind="gdn", pre=0, **kw):
+    ptrs = dict(q=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE, s0=None, cu=FAKE, o=FAKE, sf=None, ws=FAKE)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    fn = lib.gdn_prefill_ex if kind == "gdn" else lib.kda_prefill_ex
+    rc = fn(vp(ptrs["q"]), vp(ptrs["k"]), vp(ptrs["v"]), vp(ptrs["g"]), vp(ptrs["beta"]),
+            vp(ptrs["s0"]), vp(ptrs["cu"]), 1, 100, 1, 1, 64, 64, 1.0, 0, pre, vp(ptrs["o"]),
+            vp(ptrs["sf"]), vp(ptrs["ws"]), kw.get("ws_bytes", 64), None)
+    return rc, lib.hagdn_last_error().decode()
+
+
+@needs_lib
+@pytest.mark.parametrize("kind", ["gdn", "kda"])
+def test_prefill_ex_rejects_unknown_flags(kind):
+    lib = P.load_library()
+    rc, msg = _call_ex(lib, kind, pre=8)
+    assert rc == 1 and "preprocessing" in msg
+    # valid flags pass the flag check and stop at the (too small) workspace
+    assert _call_ex(lib, kind, pre=7)[0] == 3
+
+
+def _call_dec(lib, kind="gdn", N=4, Hqk=1, Hv=1, Dk=64, Dv=64, dtype=0, pre=0, num_slots=4, **over):
+    ptrs = dict(q=FAKE, k=FAKE, v=FAKE, g=FAKE, beta=FAKE, state=FAKE, slots=None, o=FAKE)
+    ptrs.update(over)
+    vp = lambda x: None if x is None else ctypes.c_void_p(x)
+    fn = lib.gdn_decode if kind == "gdn" else lib.kda_decode
+    rc = fn(vp(ptrs["q"]), vp(ptrs["k"]), vp(ptrs["v"]), vp(ptrs["g"]), vp(ptrs["beta"]),
+            vp(ptrs["state"]), vp(ptrs["slots"]), num_slots, N, Hqk, Hv, Dk, Dv, 1.0, dtype, pre,
+            vp(ptrs["o"]), None)
+    return rc, lib.hagdn_last_error().decode()
+
+
+@needs_lib
+@pytest.mark.parametrize("kind", ["gdn", "kda"])
+def test_decode_host_validation(kind):
+    lib = P.load_library()
+    EINVAL, EUNSUP = 1, 2
+    assert _call_dec(lib, kind, N=0)[0] == 0            # no-op, nothing launched
+    assert _call_dec(lib, kind, N=-1)[0] == EINVAL
+    assert _call_dec(lib, kind, state=None)[0] == EINVAL
+    assert _call_dec(lib, kind, o=None)[0] == EINVAL
+    assert _call_dec(lib, kind, Hqk=2, Hv=3)[0] == EINVAL
+    assert _call_dec(lib, kind, Dk=96)[0] == EUNSUP
+    assert _call_dec(lib, kind, dtype=5)[0] == EUNSUP
+    assert _call_dec(lib, kind, pre=16)[0] == EINVAL
+    assert _call_dec(lib, kind, state=FAKE + 4)[0] == EINVAL   # misaligned
+    assert _call_dec(lib, kind, slots=FAKE + 2)[0] == EINVAL
+    assert _call_dec(lib, kind, slots=FAKE, num_slots=0)[0] == EINVAL
