@@ -261,7 +261,7 @@ int decode(bool kda, const void *q, const void *k, const void *v, const float *g
   if (N == 0) return HAGDN_OK;
   if (!slots) num_slots = N;
   if (num_slots < 1) return fail(HAGDN_EINVAL, "num_slots must be >= 1 (got %d)", num_slots);
-  if ((size_t)N * Hv * (Dv / 32) > 0x7fffffffu) return fail(HAGDN_EINVAL, "N x Hv too large");
+  if ((size_t)N * Hv * (Dv / 64) > 0x7fffffffu) return fail(HAGDN_EINVAL, "N x Hv too large");
   if (!q || !k || !v || !g || !beta || !state || !o)
     return fail(HAGDN_EINVAL, "NULL required pointer (q, k, v, g, beta, state, o)");
   const void *p16[] = {q, k, v, o, state};

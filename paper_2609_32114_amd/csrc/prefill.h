@@ -99,7 +99,7 @@ hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStrea
 // segment-parallel path: segment maps, then ops #5 + #6 per segment
 hipError_t launch_seg_transfer(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
 hipError_t launch_seg_state(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
-// one decode step (N x Hv x Dv/32 workgroups)
+// one decode step (N x Hv x Dv/64 workgroups)
 hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool kda, hipStream_t stream);
 
 }  // namespace hagdn
