@@ -85,6 +85,9 @@ def load_library():
     """Load libhagdn.so (raises if it has not been built)."""
     global _lib
     if _lib is None:
+        # torch first: the library then binds to the HIP runtime torch loaded,
+        # so that both share one runtime (and device context) in the process
+        import torch  # noqa: F401
         if not os.path.exists(_LIB_PATH):
             raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
                                "`python -m paper_2609_32114_amd.build`")
