@@ -106,6 +106,14 @@ __device__ __forceinline__ void store4(float *p, f32x4 v) {
   *reinterpret_cast<f32x4 *>(p) = v;
 }
 
+// Eight consecutive elements from two accumulator quads (one 16-byte store
+// for bf16, two for fp32).
+__device__ __forceinline__ void store8(bf16_t *p, f32x4 lo, f32x4 hi);
+__device__ __forceinline__ void store8(float *p, f32x4 lo, f32x4 hi) {
+  *reinterpret_cast<f32x4 *>(p) = lo;
+  *reinterpret_cast<f32x4 *>(p + 4) = hi;
+}
+
 // ---------------------------------------------------- 16-byte vector access
 // A uint4 holds 8 bf16 or 4 fp32 elements; element j (compile-time after
 // unrolling) read as fp32, read raw, or packed from fp32 with rounding.
@@ -203,6 +211,10 @@ __device__ __forceinline__ void store_frag_at(bf16_t *p, bf16x8 f) {
 __device__ __forceinline__ void store_frag_at(float *p, f32x8 f) {
   *reinterpret_cast<f32x4 *>(p) = __builtin_shufflevector(f, f, 0, 1, 2, 3);
   *reinterpret_cast<f32x4 *>(p + 4) = __builtin_shufflevector(f, f, 4, 5, 6, 7);
+}
+
+__device__ __forceinline__ void store8(bf16_t *p, f32x4 lo, f32x4 hi) {
+  *reinterpret_cast<uint4 *>(p) = __builtin_bit_cast(uint4, frag_from_acc<bf16_t>(lo, hi));
 }
 
 // Store a fragment where load_frag would read it: 8 elements at p + 8*grp.

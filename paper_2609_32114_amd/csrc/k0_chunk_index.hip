@@ -29,10 +29,19 @@ __global__ __launch_bounds__(kIndexThreads) void chunk_index_kernel(PrefillArgs 
   const int32_t *cu = a.cu_seqlens;
   __shared__ int s_scan[2][kIndexThreads];
   __shared__ int s_carry[2];
+  __shared__ int4 s_info[kIndexThreads];  // the first kIndexThreads sequences' tables
+  __shared__ int2 s_seg[kIndexThreads];
 
   int bad = 0;
-  for (int n = tid; n < N; n += kIndexThreads)
-    if (cu[n + 1] < cu[n]) bad = 1;
+  int cu0 = 0, cu1 = 0;  // cu[tid], cu[tid + 1]: the first scan pass reuses them
+  for (int n = tid; n < N; n += kIndexThreads) {
+    const int x0 = cu[n], x1 = cu[n + 1];
+    if (x1 < x0) bad = 1;
+    if (n == tid) {
+      cu0 = x0;
+      cu1 = x1;
+    }
+  }
   if (tid == 0 && (cu[0] != 0 || cu[N] != a.T)) bad = 1;
   bad = __syncthreads_or(bad);
 
@@ -43,8 +52,8 @@ __global__ __launch_bounds__(kIndexThreads) void chunk_index_kernel(PrefillArgs 
     const int n = base + tid;
     int st = 0, len = 0;
     if (n < N && !bad) {
-      st = cu[n];
-      len = cu[n + 1] - st;
+      st = base == 0 ? cu0 : cu[n];
+      len = (base == 0 ? cu1 : cu[n + 1]) - st;
     }
     const int nch = (len + kChunk - 1) / kChunk;
     const int nseg = n < N ? max(1, (nch + L - 1) / L) : 0;
@@ -60,8 +69,14 @@ __global__ __launch_bounds__(kIndexThreads) void chunk_index_kernel(PrefillArgs 
       __syncthreads();
     }
     if (n < N) {
-      a.seq_info[n] = make_int4(s_carry[0] + s_scan[0][tid] - nch, nch, st, len);
-      a.seq_seg[n] = make_int2(s_carry[1] + s_scan[1][tid] - nseg, nseg);
+      const int4 si = make_int4(s_carry[0] + s_scan[0][tid] - nch, nch, st, len);
+      const int2 ss = make_int2(s_carry[1] + s_scan[1][tid] - nseg, nseg);
+      a.seq_info[n] = si;
+      a.seq_seg[n] = ss;
+      if (base == 0) {
+        s_info[tid] = si;
+        s_seg[tid] = ss;
+      }
     }
     __syncthreads();
     if (tid == kIndexThreads - 1) {
@@ -71,6 +86,10 @@ __global__ __launch_bounds__(kIndexThreads) void chunk_index_kernel(PrefillArgs 
     __syncthreads();
   }
   int total = s_carry[0], total_segs = s_carry[1];
+  // a batch of at most kIndexThreads sequences keeps its tables in LDS (one
+  // scan pass): the chunk and segment loops below then search LDS instead of
+  // reading the tables back from memory
+  const bool lds_tables = N <= kIndexThreads;
   // cannot happen for a valid batch; keeps every later index in range anyway
   if (total > a.max_chunks || total_segs > a.max_segs) {
     bad = 1;
@@ -79,6 +98,10 @@ __global__ __launch_bounds__(kIndexThreads) void chunk_index_kernel(PrefillArgs 
     for (int n = tid; n < N; n += kIndexThreads) {
       a.seq_info[n] = make_int4(0, 0, 0, 0);
       a.seq_seg[n] = make_int2(n, 1);
+      if (n < kIndexThreads) {
+        s_info[n] = make_int4(0, 0, 0, 0);
+        s_seg[n] = make_int2(n, 1);
+      }
     }
   }
   __threadfence_block();
@@ -92,9 +115,9 @@ __global__ __launch_bounds__(kIndexThreads) void chunk_index_kernel(PrefillArgs 
       int lo = 0, hi = N - 1;
       while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (a.seq_info[mid].x <= c) lo = mid; else hi = mid - 1;
+        if ((lds_tables ? s_info[mid].x : a.seq_info[mid].x) <= c) lo = mid; else hi = mid - 1;
       }
-      const int4 s = a.seq_info[lo];
+      const int4 s = lds_tables ? s_info[lo] : a.seq_info[lo];
       const int j = c - s.x;
       if (j >= 0 && j < s.y) {
         const int off = j * kChunk;
@@ -110,12 +133,12 @@ __global__ __launch_bounds__(kIndexThreads) void chunk_index_kernel(PrefillArgs 
       int lo = 0, hi = N - 1;
       while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
-        if (a.seq_seg[mid].x <= sg) lo = mid; else hi = mid - 1;
+        if ((lds_tables ? s_seg[mid].x : a.seq_seg[mid].x) <= sg) lo = mid; else hi = mid - 1;
       }
-      const int2 ss = a.seq_seg[lo];
+      const int2 ss = lds_tables ? s_seg[lo] : a.seq_seg[lo];
       const int j = sg - ss.x;
       if (j >= 0 && j < ss.y) {
-        const int4 s = a.seq_info[lo];
+        const int4 s = lds_tables ? s_info[lo] : a.seq_info[lo];
         info = make_int4(lo, s.x + j * L, min(L, s.y - j * L), j);
       }
     }

@@ -379,11 +379,12 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 #pragma unroll
       for (int kb = 0; kb < DK / 32; ++kb) {
         float xk[8], xq[8];
+        const Frag<T> kraw = frag_sw<L::LDK>(sK, r, kb * 32 + 8 * grp);  // channels kc(grp, 0..7)
 #pragma unroll
         for (int jj = 0; jj < 8; ++jj) {
           const int d = kb * 32 + kc(grp, jj);
           const float ex = __expf(sGam[r * L::LDG + d] - sGam[rho * L::LDG + d]);
-          xk[jj] = E::to_f32(sK[swz<T, L::LDK>(r, d)]) * ex;
+          xk[jj] = frag_elem(kraw, jj) * ex;
           xq[jj] = frag_elem(qf[kb], jj) * ex;
         }
         kr[kb] = make_frag<T>(xk);
@@ -396,10 +397,11 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 #pragma unroll
           for (int kb = 0; kb < DK / 32; ++kb) {
             float xs[8];
+            const Frag<T> sraw = frag_sw<L::LDK>(sK, sb, kb * 32 + 8 * grp);
 #pragma unroll
             for (int jj = 0; jj < 8; ++jj) {
               const int d = kb * 32 + kc(grp, jj);
-              xs[jj] = E::to_f32(sK[swz<T, L::LDK>(sb, d)]) * __expf(sGam[rho * L::LDG + d] - sGam[sb * L::LDG + d]);
+              xs[jj] = frag_elem(sraw, jj) * __expf(sGam[rho * L::LDG + d] - sGam[sb * L::LDG + d]);
             }
             const Frag<T> ks = make_frag<T>(xs);
             accA[j] = mma(accA[j], ks, kr[kb]);
@@ -524,10 +526,11 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
           kf = frag_sw<L::LDT>(sKt, d, kb * 32 + 8 * grp);
         } else {
           float xk[8];
+          const Frag<T> kraw = frag_sw<L::LDT>(sKt, d, kb * 32 + 8 * grp);  // tokens kc(grp, 0..7)
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             const int s = kb * 32 + kc(grp, j);
-            xk[j] = E::to_f32(sKt[swz<T, L::LDT>(d, s)]) * __expf(sGam[s * L::LDG + d]);
+            xk[j] = frag_elem(kraw, j) * __expf(sGam[s * L::LDG + d]);
           }
           kf = make_frag<T>(xk);
         }
@@ -582,14 +585,19 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) bk[kb] = frag_sw<L::LDT>(sKt, 16 * n + col, kb * 32 + 8 * grp);
 #pragma unroll
-      for (int m = 0; m < KT; ++m) {
-        f32x4 acc = zero4();
+      for (int m2 = 0; m2 < KT; m2 += 2) {
+        f32x4 acc[2];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-          acc = mma(acc, frag_sw<L::LDT>(sWt, 16 * m + col, kb * 32 + 8 * grp), bk[kb]);
+        for (int h = 0; h < 2; ++h) {
+          acc[h] = zero4();
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+            acc[h] = mma(acc[h], frag_sw<L::LDT>(sWt, 16 * (m2 + h) + col, kb * 32 + 8 * grp), bk[kb]);
+        }
         // lane: column d_out, rows d_in = 16m + 4grp + e = 32(m >> 1) + kmap(grp, 4(m & 1) + e)
-        // -> slots 4(m & 1) + e of operand block (t = n, kb = m >> 1)
-        store4(nm_out + ((size_t)(n * (DK / 32) + (m >> 1)) * 64 + lane) * 8 + 4 * (m & 1), -acc);
+        // -> slots 4(m & 1) + e of operand block (t = n, kb = m >> 1): m = m2, m2 + 1 fill
+        // the lane's 8 slots, one 16-byte store
+        store8(nm_out + ((size_t)(n * (DK / 32) + (m2 >> 1)) * 64 + lane) * 8, -acc[0], -acc[1]);
       }
     }
     // (b) B = Kt U~, the state kernel's accumulator init (lane-major, prefill.h):
@@ -606,13 +614,21 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       Frag<T> bu[2];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) bu[kb] = frag_sw<L::LDT>(sUt, dv_of(n, col), kb * 32 + 8 * grp);
+      f32x4 acc[KPW];
 #pragma unroll
       for (int mm = 0; mm < KPW; ++mm) {
-        const int m = wave * KPW + mm;
-        f32x4 acc = zero4();
+        acc[mm] = zero4();
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) acc = mma(acc, ak[mm][kb], bu[kb]);
-        store4(b_out + ((size_t)n * 64 + lane) * (4 * KT) + 4 * m, acc);
+        for (int kb = 0; kb < 2; ++kb) acc[mm] = mma(acc[mm], ak[mm][kb], bu[kb]);
+      }
+      // this wave's KPW row tiles m are consecutive: pairs share one 16-byte store
+      T *bl = b_out + ((size_t)n * 64 + lane) * (4 * KT) + 4 * (wave * KPW);
+      if constexpr (KPW % 2 == 0) {
+#pragma unroll
+        for (int mm = 0; mm < KPW; mm += 2) store8(bl + 4 * mm, acc[mm], acc[mm + 1]);
+      } else {
+#pragma unroll
+        for (int mm = 0; mm < KPW; ++mm) store4(bl + 4 * mm, acc[mm]);
       }
     }
     // (c) Q' = Q e^gamma - P W and (d) O_loc = P U~, the output kernel's B
@@ -624,16 +640,23 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
     const int r = rq;
     T *qp_out = static_cast<T *>(a.Qp) + blk * ((size_t)kChunk * DK) + (size_t)wave * (DK / 32) * 64 * 8;
 #pragma unroll
-    for (int m = 0; m < KT; ++m) {
-      const int d = 16 * m + 4 * grp;
-      f32x4 qe = qacc[m] * qscale;
-      f32x4 acc = zero4();
+    for (int m2 = 0; m2 < KT; m2 += 2) {
+      f32x4 res[2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-        if (kb < nkb) acc = mma(acc, frag_sw<L::LDT>(sWt, 16 * m + col, kb * 32 + 8 * grp), pb[kb]);
+      for (int h = 0; h < 2; ++h) {
+        const int m = m2 + h;
+        const int d = 16 * m + 4 * grp;
+        f32x4 qe = qacc[m] * qscale;
+        f32x4 acc = zero4();
 #pragma unroll
-      for (int e = 0; e < 4; ++e) qe[e] *= KDA ? __expf(sGam[r * L::LDG + d + e]) : __expf(sGam[r]);
-      store4(qp_out + ((size_t)(m >> 1) * 64 + lane) * 8 + 4 * (m & 1), qe - acc);
+        for (int kb = 0; kb < 2; ++kb)
+          if (kb < nkb) acc = mma(acc, frag_sw<L::LDT>(sWt, 16 * m + col, kb * 32 + 8 * grp), pb[kb]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) qe[e] *= KDA ? __expf(sGam[r * L::LDG + d + e]) : __expf(sGam[r]);
+        res[h] = qe - acc;
+      }
+      // slots 4(m & 1) + e of block kb = m >> 1: m2 and m2 + 1 fill them, one 16-byte store
+      store8(qp_out + ((size_t)(m2 >> 1) * 64 + lane) * 8, res[0], res[1]);
     }
     // O_loc^T rows of state tile m: lane col feeds U~ row dv_of(m, col)
     T *ol_out = static_cast<T *>(a.Ol) + blk * ((size_t)kChunk * DV);
