@@ -160,3 +160,24 @@ def test_workload3_shape_stress(variant):
 def test_workload2_shape_stress(variant):
     inp = make_workload(2, variant=variant)
     check_against_oracle(inp, heads=[4], label=f"workload2-{variant}")
+
+
+# More walk workgroups than CUs (N x Hv x Dv/16 > 256): the state walk runs its
+# two-per-CU variant with a shallower pipeline.  Long-memory gates so that the
+# state carries across every chunk; the oracle checks every head.
+WIDE = [
+    # kind, lengths, Hqk, Hv, Dk, Dv
+    ("gdn", (300, 200, 150), 8, 16, 128, 128),
+    ("kda", (300, 200, 150), 8, 16, 128, 128),
+    ("gdn", (130, 0, 260, 64, 1), 4, 16, 64, 64),
+    ("kda", (200, 129), 2, 40, 128, 64),
+    ("gdn", (129, 200), 8, 40, 64, 128),
+]
+
+
+@pytest.mark.parametrize("case", WIDE, ids=lambda c: f"{c[0]}-N{len(c[1])}-Hv{c[3]}-d{c[4]}x{c[5]}")
+def test_many_walks(case):
+    kind, lengths, Hqk, Hv, Dk, Dv = case
+    assert len(lengths) * Hv * (Dv // 16) > 256
+    inp = make_case(kind, lengths, Hqk, Hv, Dk, Dv, "bf16", with_s0=True, variant="lm", seed=31)
+    check_against_oracle(inp, label="many-walks")
