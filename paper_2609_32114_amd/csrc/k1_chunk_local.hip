@@ -108,7 +108,7 @@ __device__ __forceinline__ LocalItem local_item(const PrefillArgs &a, int item) 
   return it;
 }
 
-// Global inputs of one item, loaded one item ahead (padded tokens: zeros).
+// Global inputs of one item (padded tokens: zeros).
 // Every load is issued unconditionally from a row clamped into the chunk and
 // the padding is selected away afterwards, so the memory counters stay exact.
 template <typename T, int DK, int DV, bool KDA, bool PRE>
@@ -223,14 +223,6 @@ struct LocalIn {
   }
 };
 
-// Persistent where registers allow two workgroups per CU alongside the
-// next item's inputs (GDN bf16): workgroup b takes items b, b + gridDim.x, ...
-// (chunk-major, so past the last chunk every later item is empty too) and
-// loads item n+1's inputs while it computes item n.  Otherwise one workgroup
-// per item.
-template <typename T, bool KDA>
-constexpr bool local_persistent() { return false; }
-
 // PRE: the call carries preprocessing flags (a separate instance, so that the
 // plain path keeps its register budget).
 template <typename T, int DK, int DV, bool KDA, bool PRE>
@@ -244,18 +236,11 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
   constexpr int KPW = KT / 4;             // d_k tiles per wave in the reduce-side products
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
-  constexpr bool kKvgAhead = local_persistent<T, KDA>();
-  constexpr bool kQAhead = local_persistent<T, KDA>();
-  int item = blockIdx.x;
-  LocalItem cur = local_item(a, item);
-  if (cur.len <= 0) return;
+  const LocalItem cur = local_item(a, blockIdx.x);
+  if (cur.len <= 0) return;  // past the last chunk: uniform for the workgroup
   In in;
-  if constexpr (kKvgAhead) in.load_kvg(a, cur);
-  if constexpr (kQAhead) in.load_q(a, cur);
-  for (;;) {
-  const LocalItem nxt = local_item(a, item + gridDim.x);
-  if constexpr (!kKvgAhead) in.load_kvg(a, cur);
-  if constexpr (!kQAhead) in.load_q(a, cur);
+  in.load_kvg(a, cur);
+  in.load_q(a, cur);
   const int c = cur.c, h = cur.h, start = cur.start, len = cur.len;
   const size_t blk = (size_t)c * a.Hv + h;
 
@@ -326,9 +311,6 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
     for (int u = 0; u < GPT; ++u) sGam[(seg * GPT + u) * L::LDG + d] = gk[u] + off;
   }
   __syncthreads();
-  // keys, values, gates and betas of this item are staged: the next item's
-  // load now, behind this item's products
-  if (kKvgAhead && nxt.len > 0) in.load_kvg(a, nxt);
 
   // ---- op #2, transposed: wave i owns tokens r in [16i, 16i+16) as the
   //      columns of A^T and P^T and computes the row blocks s = 16j.. (j <= i).
@@ -669,50 +651,33 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       store4(ol_out + ((size_t)m * 64 + lane) * 16 + 4 * wave, acc);
     }
   }
-  if (!local_persistent<T, KDA>() || nxt.len <= 0) break;  // uniform: chunk-major items
-  if constexpr (kQAhead) in.load_q(a, nxt);
-  __syncthreads();  // the next item's staging overwrites every LDS region
-  item += gridDim.x;
-  cur = nxt;
-  }  // item loop
 }
 
-// Resident workgroups per device for the persistent grid: CUs x workgroups
-// that fit on one CU (LDS and registers), looked up once per device.
+// The kernel's dynamic LDS exceeds the default 64 KiB limit for some
+// instances: raise it once per device.
 template <typename T, int DK, int DV, bool KDA, bool PRE>
-static hipError_t resident_groups(int *out) {
+static hipError_t set_lds_limit() {
   using L = LocalLayout<T, DK, DV, KDA>;
   constexpr int kMaxDevices = 64;
-  static std::atomic<int> cache[kMaxDevices];
+  static std::atomic<bool> done[kMaxDevices];
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  const int slot = dev < kMaxDevices ? dev : kMaxDevices - 1;
-  int n = dev < kMaxDevices ? cache[slot].load(std::memory_order_relaxed) : 0;
-  if (n == 0) {
-    const void *kern = reinterpret_cast<const void *>(&chunk_local_kernel<T, DK, DV, KDA, PRE>);
-    if ((e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::bytes)) != hipSuccess)
-      return e;
-    int cus = 0, per_cu = 0;
-    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
-    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kLocalThreads, L::bytes)) != hipSuccess)
-      return e;
-    n = (cus > 0 ? cus : 1) * (per_cu > 0 ? per_cu : 1);
-    if (dev < kMaxDevices) cache[slot].store(n, std::memory_order_relaxed);
-  }
-  *out = n;
+  if (dev < kMaxDevices && done[dev].load(std::memory_order_relaxed)) return hipSuccess;
+  const void *kern = reinterpret_cast<const void *>(&chunk_local_kernel<T, DK, DV, KDA, PRE>);
+  if ((e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::bytes)) != hipSuccess)
+    return e;
+  if (dev < kMaxDevices) done[dev].store(true, std::memory_order_relaxed);
   return hipSuccess;
 }
 
 template <typename T, int DK, int DV, bool KDA, bool PRE>
 static hipError_t launch_local_t(const PrefillArgs &a, hipStream_t stream) {
   using L = LocalLayout<T, DK, DV, KDA>;
-  int groups = 0;
-  hipError_t e = resident_groups<T, DK, DV, KDA, PRE>(&groups);  // also sets the LDS attribute
+  hipError_t e = set_lds_limit<T, DK, DV, KDA, PRE>();
   if (e != hipSuccess) return e;
-  const long items = (long)a.max_chunks * a.Hv;
-  const long grid = local_persistent<T, KDA>() && items > groups ? groups : items;
-  hipLaunchKernelGGL((chunk_local_kernel<T, DK, DV, KDA, PRE>), dim3((unsigned)grid), dim3(kLocalThreads), L::bytes,
+  const long items = (long)a.max_chunks * a.Hv;  // one workgroup per (chunk, value head) block
+  hipLaunchKernelGGL((chunk_local_kernel<T, DK, DV, KDA, PRE>), dim3((unsigned)items), dim3(kLocalThreads), L::bytes,
                      stream, a);
   return hipGetLastError();
 }
