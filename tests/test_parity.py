@@ -125,6 +125,28 @@ def test_bad_seqlens_are_reported_not_faulted():
     assert P.device_status(ws) == P.DEV_OK
 
 
+@pytest.mark.parametrize("kind", ["gdn", "kda"])
+def test_bad_seqlens_single_sequence(kind):
+    """One sequence with malformed cu_seqlens: the kernels take its chunk
+    bounds from T, and the status word must still keep every write out."""
+    import torch
+    import paper_2609_32114_amd as P
+    inp = make_case(kind, (300,), 1, 2, 128, 128, "bf16", with_s0=True, seed=16)
+    d = to_device(inp)
+    fn = P.gdn_prefill if kind == "gdn" else P.kda_prefill
+    ws = torch.zeros(P.workspace_size(kind, 1, 300, 1, 2, 128, 128, P.HAGDN_BF16), dtype=torch.uint8,
+                     device="cuda")
+    for bad in ([0, 299], [3, 300]):
+        cu = torch.tensor(bad, dtype=torch.int32, device="cuda")
+        o = torch.full((300, 2, 128), 7.0, dtype=torch.bfloat16, device="cuda")
+        o, sf = fn(d["q"], d["k"], d["v"], d["g"], d["beta"], initial_state=d["s0"], cu_seqlens=cu,
+                   workspace=ws, out=o)
+        assert P.device_status(ws) == P.DEV_BAD_SEQLENS
+        np.testing.assert_array_equal(sf.cpu().numpy(), inp.s0)
+        assert torch.all(o == 7.0)
+    check_against_oracle(inp, label="after bad seqlens")
+
+
 def test_bitwise_deterministic():
     inp = make_case("gdn", (1000, 333), 2, 4, 128, 128, "bf16", with_s0=True, seed=8)
     d = to_device(inp)
