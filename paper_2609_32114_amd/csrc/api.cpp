@@ -21,6 +21,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <string>
@@ -61,15 +62,26 @@ constexpr int kMaxSegChunks = 1 << 20;
 // Measured on MI355X the segments pay from about 256 chunks per sequence
 // (T = 32768: 0.40 ms against 0.57 ms at L = 32); below that every sequence
 // stays one segment.  L near sqrt(2 n) balances the three terms.
-int seg_chunks(int N, int T, int Hv, int Dv) {
-  (void)Hv; (void)Dv;
+//
+// Whatever the choice (or override), L is capped so that the o rows of one
+// segment, 64 L Hv Dv elements, span less than 2 GiB: the walk kernels address
+// a segment's rows through one buffer resource with 32-bit signed byte
+// offsets.  A call whose chains do not fit one capped segment takes the
+// segmented path, whose windows then fit too.
+int seg_chunks(int N, int T, int Hv, int Dv, size_t esz) {
+  const size_t seg_rows_bytes = (size_t)hagdn::kChunk * (size_t)Hv * (size_t)Dv * esz;
+  const long cap = std::max<long>(1, (long)(((size_t)1 << 31) - 1) / (long)seg_rows_bytes);
   const int ov = g_seg_override.load(std::memory_order_relaxed);
-  if (ov > 0) return ov;
-  const long n_all = ((long)T + hagdn::kChunk - 1) / hagdn::kChunk;  // longest possible chain
-  const long n_avg = ((long)T / (N > 0 ? N : 1) + hagdn::kChunk - 1) / hagdn::kChunk;
-  if (n_avg < 256) return n_all > 0 ? (int)(n_all < kMaxSegChunks ? n_all : kMaxSegChunks) : 1;
-  const int L = (int)std::ceil(std::sqrt(2.0 * (double)n_avg));
-  return L < 32 ? 32 : L;
+  long L;
+  if (ov > 0) {
+    L = ov;
+  } else {
+    const long n_all = ((long)T + hagdn::kChunk - 1) / hagdn::kChunk;  // longest possible chain
+    const long n_avg = ((long)T / (N > 0 ? N : 1) + hagdn::kChunk - 1) / hagdn::kChunk;
+    if (n_avg < 256) L = n_all > 0 ? std::min<long>(n_all, kMaxSegChunks) : 1;
+    else L = std::max<long>(32, (long)std::ceil(std::sqrt(2.0 * (double)n_avg)));
+  }
+  return (int)std::min(L, cap);
 }
 
 bool mul_ok(size_t a, size_t b, size_t *out) { return !__builtin_mul_overflow(a, b, out); }
@@ -89,7 +101,7 @@ bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, Layout *L) {
     return false;
   }
   L->max_chunks = (int)mc;
-  L->seg_chunks = seg_chunks(N, T, Hv, Dv);
+  L->seg_chunks = seg_chunks(N, T, Hv, Dv, esz);
   const size_t ms = mc / (size_t)L->seg_chunks + (size_t)N;
   L->max_segs = (int)ms;  // <= mc
   size_t blocks, sblocks;  // (chunk, value head) and (segment, value head) blocks
@@ -425,9 +437,11 @@ int hagdn_set_segment_chunks(int chunks) {
   return HAGDN_OK;
 }
 
-int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv) {
-  if (N < 1 || T_total < 0 || Hv < 1 || Dv < 1) return fail(HAGDN_EINVAL, "bad shape"), -1;
-  return seg_chunks(N, T_total, Hv, Dv);
+int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv, int dtype) {
+  if (N < 1 || T_total < 0 || Hv < 1 || Dv < 1)
+    return fail(HAGDN_EINVAL, "bad shape"), -1;
+  if (dtype != HAGDN_F32 && dtype != HAGDN_BF16) return fail(HAGDN_EINVAL, "bad dtype %d", dtype), -1;
+  return seg_chunks(N, T_total, Hv, Dv, dtype == HAGDN_BF16 ? 2 : 4);
 }
 
 }  // extern "C"

@@ -122,6 +122,17 @@ def test_segment_length_knob():
         assert ws_one < ws_auto
         with pytest.raises(P.HagdnError):
             P.set_segment_chunks(-1)
+        # the cap: 64 L Hv Dv elements stay below 2 GiB, forced or automatic
+        import torch
+        P.set_segment_chunks(1 << 20)
+        assert P.segment_chunks(1, 4096, 16, 128) == 8191                      # bf16: 2^31 / 256 KiB
+        assert P.segment_chunks(1, 4096, 16, 128, torch.float32) == 4095       # fp32: 2^31 / 512 KiB
+        assert P.segment_chunks(1, 32832, 128, 128, torch.float32) == 511
+        assert P.segment_chunks(1, 4096, 65535, 128, torch.float32) == 1       # 64 rows: 2147450880 B
+        P.set_segment_chunks(0)
+        L = P.segment_chunks(4096, 4096 * 2048, 16, 128)   # short chains, 8M tokens: whole, then capped
+        assert L == 8191 and 64 * L * 16 * 128 * 2 < 2 ** 31 <= 64 * (L + 1) * 16 * 128 * 2
+        assert P.segment_chunks(1, 32832, 128, 128, torch.float32) == 33     # auto: ceil(sqrt(2 * 513))
     finally:
         P.set_segment_chunks(0)
     assert P.segment_chunks(1, 4096, 16, 128) == 64

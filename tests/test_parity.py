@@ -203,3 +203,42 @@ def test_many_walks(case):
     assert len(lengths) * Hv * (Dv // 16) > 256
     inp = make_case(kind, lengths, Hqk, Hv, Dk, Dv, "bf16", with_s0=True, variant="lm", seed=31)
     check_against_oracle(inp, label="many-walks")
+
+
+@pytest.mark.parametrize("forced", [False, True])
+def test_output_beyond_2gib(forced):
+    """A single sequence whose output exceeds 2 GiB (T = 32832 tokens x 128
+    value heads x d_v = 128, fp32).  The segment length is capped so that one
+    segment's output rows stay below 2 GiB (511 chunks here), so even a forced
+    single segment (L = 2^20) takes the segmented path and no byte offset
+    overflows.  Inputs are drawn on the GPU (seeded); the oracle checks the
+    last head and one in the middle."""
+    import torch
+    import oracle
+    import paper_2609_32114_amd as P
+    from gpu_harness import oracle_threads, relerr
+    T, Hqk, Hv, D = 32832, 1, 128, 128
+    assert T * Hv * D * 4 > 2 ** 31
+    gen = torch.Generator(device="cuda").manual_seed(41)
+    q = torch.nn.functional.normalize(torch.randn(T, Hqk, D, device="cuda", generator=gen), dim=-1)
+    k = torch.nn.functional.normalize(torch.randn(T, Hqk, D, device="cuda", generator=gen), dim=-1)
+    v = torch.randn(T, Hv, D, device="cuda", generator=gen)
+    g = -0.01 * torch.nn.functional.softplus(torch.randn(T, Hv, device="cuda", generator=gen))
+    beta = torch.sigmoid(torch.randn(T, Hv, device="cuda", generator=gen))
+    try:
+        P.set_segment_chunks(1 << 20 if forced else 0)
+        L = P.segment_chunks(1, T, Hv, D, torch.float32)
+        assert L == (511 if forced else 33) and 64 * L * Hv * D * 4 < 2 ** 31
+        say(f"[gpu] o beyond 2 GiB: T={T} Hv={Hv} fp32 forced={forced} L={L}")
+        o, sf = P.gdn_prefill(q, k, v, g, beta)
+        torch.cuda.synchronize()
+    finally:
+        P.set_segment_chunks(0)
+    heads = [Hv // 2, Hv - 1]
+    ro, rs = oracle.prefill("gdn", q.cpu().numpy(), k.cpu().numpy(), v[:, heads].cpu().numpy(),
+                            g[:, heads].cpu().numpy(), beta[:, heads].cpu().numpy(),
+                            nthreads=oracle_threads())
+    eo = relerr(o[:, heads].cpu().numpy(), ro)
+    es = relerr(sf[:, heads].cpu().numpy(), rs)
+    say(f"       max-rel o={eo:.3e} s={es:.3e}")
+    assert eo <= 1e-4 and es <= 1e-4
