@@ -184,10 +184,11 @@ def test_workload2_shape_stress(variant):
     check_against_oracle(inp, heads=[4], label=f"workload2-{variant}")
 
 
-# More walk workgroups than CUs (N x Hv x Dv/16 > 256): the state walk runs its
-# two-per-CU variant with a shallower pipeline.  Long-memory gates so that the
-# state carries across every chunk; the oracle checks every head.
-WIDE = [
+# More walk workgroups than CUs (N x Hv x Dv/16 > 256): walks share CUs (two
+# per CU for bf16) and the later ones start only when earlier ones finish.
+# Long-memory gates so that the state carries across every chunk; the oracle
+# checks every head.
+MANY_WALKS = [
     # kind, lengths, Hqk, Hv, Dk, Dv
     ("gdn", (300, 200, 150), 8, 16, 128, 128),
     ("kda", (300, 200, 150), 8, 16, 128, 128),
@@ -197,7 +198,7 @@ WIDE = [
 ]
 
 
-@pytest.mark.parametrize("case", WIDE, ids=lambda c: f"{c[0]}-N{len(c[1])}-Hv{c[3]}-d{c[4]}x{c[5]}")
+@pytest.mark.parametrize("case", MANY_WALKS, ids=lambda c: f"{c[0]}-N{len(c[1])}-Hv{c[3]}-d{c[4]}x{c[5]}")
 def test_many_walks(case):
     kind, lengths, Hqk, Hv, Dk, Dv = case
     assert len(lengths) * Hv * (Dv // 16) > 256
