@@ -53,15 +53,21 @@ constexpr int kDecodeKernel = 4;
 // Chunks per segment of the state chain; 0 = chosen per call (seg_chunks).
 std::atomic<int> g_seg_override{0};
 constexpr int kMaxSegChunks = 1 << 20;
+constexpr long kCus = 256;  // compute units of an MI355X (gfx950)
 
 // Segment length for a batch of N sequences over T tokens.  A chain of n
-// chunks walked whole costs n dependent steps on 8 CUs per head; cut into
-// segments of L it costs about L (segment maps) + n / L (prefix) + L (walk)
-// steps of a head-resident workgroup, each about three times as long (it
-// moves a whole head's operands through one CU), plus twice the matrix work.
-// Measured on MI355X the segments pay from about 256 chunks per sequence
-// (T = 32768: 0.40 ms against 0.57 ms at L = 32); below that every sequence
-// stays one segment.  L near sqrt(2 n) balances the three terms.
+// chunks walked whole costs n dependent steps; its workgroups (one per
+// sequence, value head and 16-column tile) occupy N Hv Dv/16 CUs.  Cut into
+// segments of L, it costs about L steps for the segment maps, n / L for the
+// prefix and L for the walk, each step about three times as long (one
+// head-resident workgroup moves a whole head's operands through one CU), on
+// about (n / L) Hv workgroups.  Measured on MI355X (1 sequence, d = 128, bf16,
+// operator totals): with 16 heads (128 walk workgroups) segments pay from
+// about 144 chunks (T = 9216: 217 us at L = 16 against 248 whole; T = 12288:
+// 286 against 349; T = 32768: 694 against 855), and the best L puts about
+// one segment workgroup on every CU (L = n Hv / 256, at least 12).  With 32
+// heads (256 walk workgroups) the whole walk still won at 256 chunks (604 us
+// against 682), so the threshold grows with the walks' share of the CUs.
 //
 // Whatever the choice (or override), L is capped so that the o rows of one
 // segment, 64 L Hv Dv elements, span less than 2 GiB: the walk kernels address
@@ -78,8 +84,10 @@ int seg_chunks(int N, int T, int Hv, int Dv, size_t esz) {
   } else {
     const long n_all = ((long)T + hagdn::kChunk - 1) / hagdn::kChunk;  // longest possible chain
     const long n_avg = ((long)T / (N > 0 ? N : 1) + hagdn::kChunk - 1) / hagdn::kChunk;
-    if (n_avg < 256) L = n_all > 0 ? std::min<long>(n_all, kMaxSegChunks) : 1;
-    else L = std::max<long>(32, (long)std::ceil(std::sqrt(2.0 * (double)n_avg)));
+    const double walks = (double)(N > 0 ? N : 1) * Hv * std::max(1, Dv / 16);
+    const double threshold = 144.0 * std::max(1.0, walks / (kCus / 2));
+    if ((double)n_avg < threshold) L = n_all > 0 ? std::min<long>(n_all, kMaxSegChunks) : 1;
+    else L = std::max<long>(12, (n_all * Hv + kCus - 1) / kCus);
   }
   return (int)std::min(L, cap);
 }

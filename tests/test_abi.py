@@ -102,12 +102,19 @@ def test_segment_length_knob():
     import paper_2609_32114_amd as P
     P.load_library()
     try:
-        # automatic: short chains stay one segment, long ones get about sqrt(2 n)
+        # automatic: short chains stay one segment; long ones get about one
+        # segment workgroup per CU (n Hv / 256 chunks, at least 12)
         assert P.segment_chunks(1, 256, 1, 64) == 4
         assert P.segment_chunks(1, 0, 1, 64) == 1
         assert P.segment_chunks(1, 4096, 16, 128) == 64
+        assert P.segment_chunks(1, 9151, 16, 128) == 143    # below 144 chunks: whole
+        assert P.segment_chunks(1, 9216, 16, 128) == 12     # 144 chunks
+        assert P.segment_chunks(1, 12288, 16, 128) == 12
+        assert P.segment_chunks(1, 16384, 16, 128) == 16
         assert P.segment_chunks(1, 32768, 16, 128) == 32
-        assert P.segment_chunks(1, 131072, 16, 128) == 64   # 2048 chunks
+        assert P.segment_chunks(1, 131072, 16, 128) == 128  # 2048 chunks
+        assert P.segment_chunks(1, 16384, 32, 128) == 256   # 256 walk workgroups: threshold 288
+        assert P.segment_chunks(1, 18432, 32, 128) == 36    # 288 chunks: 288 x 32 / 256
         assert P.segment_chunks(8, 34816, 32, 128) == 544   # short average chains: whole
         P.set_segment_chunks(8)
         auto = P.segment_chunks(1, 4096, 16, 128)
@@ -132,7 +139,7 @@ def test_segment_length_knob():
         P.set_segment_chunks(0)
         L = P.segment_chunks(4096, 4096 * 2048, 16, 128)   # short chains, 8M tokens: whole, then capped
         assert L == 8191 and 64 * L * 16 * 128 * 2 < 2 ** 31 <= 64 * (L + 1) * 16 * 128 * 2
-        assert P.segment_chunks(1, 32832, 128, 128, torch.float32) == 33     # auto: ceil(sqrt(2 * 513))
+        assert P.segment_chunks(1, 32832, 128, 128, torch.float32) == 511    # whole (1024 walks), capped
     finally:
         P.set_segment_chunks(0)
     assert P.segment_chunks(1, 4096, 16, 128) == 64

@@ -206,14 +206,15 @@ def test_many_walks(case):
     check_against_oracle(inp, label="many-walks")
 
 
-@pytest.mark.parametrize("forced", [False, True])
+@pytest.mark.parametrize("forced", [0, 32])
 def test_output_beyond_2gib(forced):
     """A single sequence whose output exceeds 2 GiB (T = 32832 tokens x 128
-    value heads x d_v = 128, fp32).  The segment length is capped so that one
-    segment's output rows stay below 2 GiB (511 chunks here), so even a forced
-    single segment (L = 2^20) takes the segmented path and no byte offset
-    overflows.  Inputs are drawn on the GPU (seeded); the oracle checks the
-    last head and one in the middle."""
+    value heads x d_v = 128, fp32).  The automatic choice would walk the chain
+    whole (1024 walk workgroups), but the segment length is capped so that one
+    segment's output rows stay below 2 GiB (511 chunks here): the call takes
+    the segmented path with two segments and no byte offset overflows.  A
+    forced L = 32 covers many segments at this size.  Inputs are drawn on the
+    GPU (seeded); the oracle checks the last head and one in the middle."""
     import torch
     import oracle
     import paper_2609_32114_amd as P
@@ -227,9 +228,9 @@ def test_output_beyond_2gib(forced):
     g = -0.01 * torch.nn.functional.softplus(torch.randn(T, Hv, device="cuda", generator=gen))
     beta = torch.sigmoid(torch.randn(T, Hv, device="cuda", generator=gen))
     try:
-        P.set_segment_chunks(1 << 20 if forced else 0)
+        P.set_segment_chunks(forced)
         L = P.segment_chunks(1, T, Hv, D, torch.float32)
-        assert L == (511 if forced else 33) and 64 * L * Hv * D * 4 < 2 ** 31
+        assert L == (forced or 511) and 64 * L * Hv * D * 4 < 2 ** 31
         say(f"[gpu] o beyond 2 GiB: T={T} Hv={Hv} fp32 forced={forced} L={L}")
         o, sf = P.gdn_prefill(q, k, v, g, beta)
         torch.cuda.synchronize()
