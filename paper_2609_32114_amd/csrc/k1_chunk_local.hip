@@ -72,25 +72,55 @@ __device__ __forceinline__ f32x8 frag_sw(const float *t, int r, int e) {
 //   X  sK  [64][DK]  keys, token rows (op #2)   -> sKt [DK][64] keys, channel rows (op #4 on)
 //   Y  sA  [64][64]  A, then T (fp32, ops #2-#3) -> sWt [DK][64] W, channel rows
 //   Z  sVt [DV][64]  values, channel rows         -> sUt [DV][64] U~, channel rows
-// all XOR-swizzled; plus beta, the GDN decay column and the gate scan.
+// all XOR-swizzled; plus the gate scan gamma.  GDN also keeps beta and its
+// decay column e^(gamma_last - gamma_s) here.  KDA's gamma is a [64][DK]
+// table, so a KDA item holds beta in registers and runs its gate-scan totals
+// through region Y (free until op #2): at d_k = d_v = 128, bf16, that keeps
+// the item at exactly 80 KiB, two per CU.
 template <typename T, int DK, int DV, bool KDA>
 struct LocalLayout {
   static constexpr int LDK = DK;       // sK row length
   static constexpr int LDT = kChunk;   // channel-row length (sKt, sWt, sVt, sUt)
   static constexpr int LDA = kChunk;   // sA row length
-  static constexpr int LDG = KDA ? DK + 1 : 1;  // sGam [64][LDG] (GDN: [64])
   static constexpr size_t bytesX = sizeof(T) * kChunk * DK;
   static constexpr size_t bytesY = sizeof(float) * kChunk * kChunk > sizeof(T) * DK * kChunk
                                        ? sizeof(float) * kChunk * kChunk : sizeof(T) * DK * kChunk;
   static constexpr size_t off_K = 0;   // region X
   static constexpr size_t off_A = off_K + bytesX;   // region Y
   static constexpr size_t off_Vt = off_A + bytesY;  // region Z
-  static constexpr size_t off_beta = off_Vt + sizeof(T) * DV * kChunk;
-  static constexpr size_t off_kdec = off_beta + sizeof(float) * kChunk;  // GDN e^(gamma_last - gamma_s)
-  static constexpr size_t off_tot = off_kdec + sizeof(float) * kChunk;   // KDA gate-scan segment totals
-  static constexpr size_t off_gam = off_tot + sizeof(float) * (KDA ? kLocalThreads : 0);
-  static constexpr size_t bytes = off_gam + sizeof(float) * kChunk * LDG;
+  static constexpr size_t off_beta = off_Vt + sizeof(T) * DV * kChunk;                // GDN
+  static constexpr size_t off_kdec = off_beta + (KDA ? 0 : sizeof(float) * kChunk);   // GDN
+  static constexpr size_t off_gam = off_kdec + (KDA ? 0 : sizeof(float) * kChunk);
+  static constexpr size_t bytes = off_gam + sizeof(float) * kChunk * (KDA ? DK : 1);
+  // KDA gate-scan segment totals: kLocalThreads floats in region Y, behind the
+  // kLocalThreads-float scratch of the q/k normalisation
+  static constexpr size_t off_tot = off_A + sizeof(float) * kLocalThreads;
+  static_assert(!KDA || off_tot + sizeof(float) * kLocalThreads <= off_A + bytesY, "totals fit region Y");
 };
+
+// KDA gamma[r][d] in the [64][DK] table, rows unpadded: the 16-byte chunk q of
+// row r is stored at chunk q ^ f(r), f(r) = (r & 7) ^ 4 ((r >> 3) & 1).  The
+// (r & 7) term lets eight consecutive token rows read the same channels as
+// 16-byte vectors with no bank conflict (op #2, Q'); the second term puts
+// token rows 8 apart into different halves of a 32-channel block, so the
+// per-element reads of op #4 (16 channels x 4 token rows 8 apart) conflict at
+// most 2-way.  Chunks move only inside their 32-channel block.
+template <int DK>
+__device__ __forceinline__ int gam_at(int r, int d) {
+  const int f = (r & 7) ^ (((r >> 3) & 1) << 2);
+  return r * DK + ((((d >> 2) ^ f) << 2) | (d & 3));
+}
+// gamma[r][d .. d+7] (d a multiple of 8) as two 16-byte reads
+template <int DK>
+__device__ __forceinline__ void gam8(const float *g, int r, int d, float (&x)[8]) {
+  const f32x4 lo = *reinterpret_cast<const f32x4 *>(g + gam_at<DK>(r, d));
+  const f32x4 hi = *reinterpret_cast<const f32x4 *>(g + gam_at<DK>(r, d + 4));
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    x[e] = lo[e];
+    x[4 + e] = hi[e];
+  }
+}
 
 // One (chunk, value head) work item: chunk c = item / Hv, head h = item % Hv.
 struct LocalItem {
@@ -117,7 +147,7 @@ struct LocalIn {
   static constexpr int NKV = DK / 4 / V, NVV = DV / 4 / V;       // 16-byte vectors per lane
   static constexpr int GPT = KDA ? kChunk * DK / kLocalThreads : 1;  // gate values per thread
   u32x4 kv[NKV], vv[NVV];  // keys, values: lane = token, wave = channel quarter
-  float bval, gk[GPT];     // beta of token tid; gates (KDA: thread = (channel, token segment))
+  float bval, gk[GPT];     // beta of token tid (KDA: of token 16 wave + col); gates (KDA: thread = (channel, token segment))
   Frag<T> qf[DK / 32];     // queries of token 16 wave + col, op #2 operand
   f32x4 qacc[DK / 16];     // the same queries in accumulator layout (channels 16m + 4grp ..)
 
@@ -140,10 +170,13 @@ struct LocalIn {
       const u32x4 x = *reinterpret_cast<const u32x4 *>(vb + i * V);
       vv[i] = live ? x : u32x4{0, 0, 0, 0};
     }
-    const int rt = min(tid & (kChunk - 1), last);
-    const float b = a.beta[(size_t)(it.start + rt) * a.Hv + it.h];
+    // GDN: thread tid < 64 holds beta of token tid (staged in LDS); KDA: each
+    // lane holds beta of its op #2 token 16 wave + col
+    const int bt = KDA ? 16 * wave + (lane & 15) : tid;
+    const float b = a.beta[(size_t)(it.start + min(bt & (kChunk - 1), last)) * a.Hv + it.h];
     const float bx = (PRE && (a.pre & kPreBetaSigmoid)) ? sigmoid(b) : b;
-    bval = (tid < kChunk && tid < it.len) ? bx : 0.f;
+    bval = (bt < kChunk && bt < it.len) ? bx : 0.f;
+    const int rt = min(tid & (kChunk - 1), last);
     if constexpr (KDA) {
       const int d = tid % DK, seg = tid / DK;
       const float *gb = a.g + ((size_t)it.start * a.Hv + it.h) * DK + d;
@@ -226,7 +259,7 @@ struct LocalIn {
 // PRE: the call carries preprocessing flags (a separate instance, so that the
 // plain path keeps its register budget).
 template <typename T, int DK, int DV, bool KDA, bool PRE>
-__global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void chunk_local_kernel(PrefillArgs a) {
   using L = LocalLayout<T, DK, DV, KDA>;
   using E = Elt<T>;
   using V16 = Vec16<T>;
@@ -287,7 +320,9 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
     for (int j = 0; j < V; ++j) sVt[swz<T, L::LDT>(cv + j, lane)] = V16::raw(u, j);
   }
   // ---- op #1: beta and gamma (inclusive cumulative log-gate)
-  if (tid < kChunk) sBeta[tid] = bval;
+  if constexpr (!KDA) {
+    if (tid < kChunk) sBeta[tid] = bval;
+  }
   if constexpr (!KDA) {
     if (wave == 0) {
       float x = gk[0];
@@ -308,7 +343,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
     float off = 0.f;
     for (int s2 = 0; s2 < seg; ++s2) off += sTot[s2 * DK + d];
 #pragma unroll
-    for (int u = 0; u < GPT; ++u) sGam[(seg * GPT + u) * L::LDG + d] = gk[u] + off;
+    for (int u = 0; u < GPT; ++u) sGam[gam_at<DK>(seg * GPT + u, d)] = gk[u] + off;
   }
   __syncthreads();
 
@@ -360,12 +395,13 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       Frag<T> kr[DK / 32], qr[DK / 32];
 #pragma unroll
       for (int kb = 0; kb < DK / 32; ++kb) {
-        float xk[8], xq[8];
+        float xk[8], xq[8], gr[8], gh[8];
         const Frag<T> kraw = frag_sw<L::LDK>(sK, r, kb * 32 + 8 * grp);  // channels kc(grp, 0..7)
+        gam8<DK>(sGam, r, kb * 32 + kc(grp, 0), gr);
+        gam8<DK>(sGam, rho, kb * 32 + kc(grp, 0), gh);
 #pragma unroll
         for (int jj = 0; jj < 8; ++jj) {
-          const int d = kb * 32 + kc(grp, jj);
-          const float ex = __expf(sGam[r * L::LDG + d] - sGam[rho * L::LDG + d]);
+          const float ex = __expf(gr[jj] - gh[jj]);
           xk[jj] = frag_elem(kraw, jj) * ex;
           xq[jj] = frag_elem(qf[kb], jj) * ex;
         }
@@ -378,13 +414,12 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
           const int sb = 16 * j + col;
 #pragma unroll
           for (int kb = 0; kb < DK / 32; ++kb) {
-            float xs[8];
+            float xs[8], gh[8], gs[8];
             const Frag<T> sraw = frag_sw<L::LDK>(sK, sb, kb * 32 + 8 * grp);
+            gam8<DK>(sGam, rho, kb * 32 + kc(grp, 0), gh);
+            gam8<DK>(sGam, sb, kb * 32 + kc(grp, 0), gs);
 #pragma unroll
-            for (int jj = 0; jj < 8; ++jj) {
-              const int d = kb * 32 + kc(grp, jj);
-              xs[jj] = frag_elem(sraw, jj) * __expf(sGam[rho * L::LDG + d] - sGam[sb * L::LDG + d]);
-            }
+            for (int jj = 0; jj < 8; ++jj) xs[jj] = frag_elem(sraw, jj) * __expf(gh[jj] - gs[jj]);
             const Frag<T> ks = make_frag<T>(xs);
             accA[j] = mma(accA[j], ks, kr[kb]);
             accP[j] = mma(accP[j], ks, qr[kb]);
@@ -396,7 +431,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int s = 16 * j + 4 * grp + e;
-          accA[j][e] = (j <= i && s < r) ? sBeta[r] * accA[j][e] : 0.f;
+          accA[j][e] = (j <= i && s < r) ? bval * accA[j][e] : 0.f;  // bval: beta of token r
           accP[j][e] = (j <= i && s <= r) ? accP[j][e] * qscale : 0.f;
         }
         *reinterpret_cast<f32x4 *>(sA + swz<float, L::LDA>(r, 16 * j + 4 * grp)) = accA[j];
@@ -404,6 +439,20 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
     }
   }
   __syncthreads();
+  // KDA: beta of the tokens this lane scales T's columns by in op #4 (no LDS
+  // copy: the gate table fills it); loaded here, used after the solve
+  float bs[KDA ? 2 : 1][8];
+  if constexpr (KDA) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int s = kb * 32 + kc(grp, j);
+        const float b = a.beta[(size_t)(start + min(s, len - 1)) * a.Hv + h];
+        const float bx = (PRE && (a.pre & kPreBetaSigmoid)) ? sigmoid(b) : b;
+        bs[kb][j] = s < len ? bx : 0.f;
+      }
+  }
   // keys as channel rows over the token rows op #2 is done with (region X)
 #pragma unroll
   for (int it = 0; it < NKV; ++it) {
@@ -479,7 +528,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int s = kb * 32 + kc(grp, j);
-        const float t = trow[j] * sBeta[s];
+        const float t = trow[j] * (KDA ? bs[kb][j] : sBeta[s]);
         xu[j] = t;
         xw[j] = KDA ? t : t * __expf(sGam[s]);
       }
@@ -512,7 +561,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             const int s = kb * 32 + kc(grp, j);
-            xk[j] = frag_elem(kraw, j) * __expf(sGam[s * L::LDG + d]);
+            xk[j] = frag_elem(kraw, j) * __expf(sGam[gam_at<DK>(s, d)]);
           }
           kf = make_frag<T>(xk);
         }
@@ -538,7 +587,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
       for (int j = 0; j < V; ++j) {
         const int p = u * V + j;
         const int s = (p & ~31) + kmap((p & 31) >> 3, p & 7);
-        const float ex = KDA ? __expf(sGam[(kChunk - 1) * L::LDG + d] - sGam[s * L::LDG + d]) : sKdec[s];
+        const float ex = KDA ? __expf(sGam[gam_at<DK>(kChunk - 1, d)] - sGam[gam_at<DK>(s, d)]) : sKdec[s];
         outv[j] = V16::get(row[s / V], s % V) * ex;
       }
       *reinterpret_cast<uint4 *>(sKt + swz<T, L::LDT>(d, u * V)) = V16::pack(outv);
@@ -547,7 +596,7 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
   {  // chunk decay e^gamma_last
     float *dec_out = a.dec + blk * DK;
     if constexpr (KDA) {
-      if (tid < DK) dec_out[tid] = __expf(sGam[(kChunk - 1) * L::LDG + tid]);
+      if (tid < DK) dec_out[tid] = __expf(sGam[gam_at<DK>(kChunk - 1, tid)]);
     } else {
       if (tid == 0) dec_out[0] = __expf(sGam[kChunk - 1]);
     }
@@ -629,12 +678,13 @@ __global__ __launch_bounds__(kLocalThreads) void chunk_local_kernel(PrefillArgs 
         const int m = m2 + h;
         const int d = 16 * m + 4 * grp;
         f32x4 qe = qacc[m] * qscale;
+        const f32x4 gq = KDA ? *reinterpret_cast<const f32x4 *>(sGam + gam_at<DK>(r, d)) : zero4();
         f32x4 acc = zero4();
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
           if (kb < nkb) acc = mma(acc, frag_sw<L::LDT>(sWt, 16 * m + col, kb * 32 + 8 * grp), pb[kb]);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) qe[e] *= KDA ? __expf(sGam[r * L::LDG + d + e]) : __expf(sGam[r]);
+        for (int e = 0; e < 4; ++e) qe[e] *= KDA ? __expf(gq[e]) : __expf(sGam[r]);
         res[h] = qe - acc;
       }
       // slots 4(m & 1) + e of block kb = m >> 1: m2 and m2 + 1 fill them, one 16-byte store
