@@ -234,6 +234,7 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   a.seg_info = reinterpret_cast<int4 *>(w + L.seg_info);
   a.Aseg = w + L.Aseg;
   a.Bseg = reinterpret_cast<float *>(w + L.Bseg);
+  a.single = N == 1 ? 1 : 0;  // the kernels derive a single sequence's tables themselves
   const bool maps = (T + hagdn::kChunk - 1) / hagdn::kChunk > L.seg_chunks;
 
   hipStream_t st = static_cast<hipStream_t>(stream_);
@@ -254,8 +255,10 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
 
   hipError_t e;
   if ((e = mark(0)) != hipSuccess) goto hip_fail;
-  if ((e = hagdn::launch_chunk_index(a, st)) != hipSuccess) goto hip_fail;
-  if ((e = mark(1)) != hipSuccess) goto hip_fail;
+  if (!a.single) {
+    if ((e = hagdn::launch_chunk_index(a, st)) != hipSuccess) goto hip_fail;
+    if ((e = mark(1)) != hipSuccess) goto hip_fail;
+  }
   if ((e = hagdn::launch_chunk_local(a, bf16, kda, st)) != hipSuccess) goto hip_fail;
   if ((e = mark(2)) != hipSuccess) goto hip_fail;
   if (maps) {

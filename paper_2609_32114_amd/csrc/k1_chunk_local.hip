@@ -131,9 +131,14 @@ __device__ __forceinline__ LocalItem local_item(const PrefillArgs &a, int item) 
   if (item < a.max_chunks * a.Hv) {
     it.c = item / a.Hv;
     it.h = item % a.Hv;
-    const int4 ci = a.chunk_info[it.c];
-    it.start = ci.y;
-    it.len = ci.z;
+    if (a.single) {  // chunk c of the only sequence (tokens [0, T))
+      it.start = it.c * kChunk;
+      it.len = max(0, min(kChunk, a.T - it.start));
+    } else {
+      const int4 ci = a.chunk_info[it.c];
+      it.start = ci.y;
+      it.len = ci.z;
+    }
   }
   return it;
 }

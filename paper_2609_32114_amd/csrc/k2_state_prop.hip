@@ -115,6 +115,7 @@ __global__ __launch_bounds__(64 * (DK / 32), sizeof(T) == 2 ? 2 : 1) void state_
   constexpr int NW = DK / 32;   // waves per chain
   constexpr int NT = DV / 16;   // d_v tiles per head
   constexpr int D = pipe_depth<T, KDA>();
+  single_status(a);
   const int b = blockIdx.x;
   const int xcd = b % kXcds, slot = b / kXcds;
   const int pair = (slot / NT) * kXcds + xcd;
@@ -125,7 +126,7 @@ __global__ __launch_bounds__(64 * (DK / 32), sizeof(T) == 2 ? 2 : 1) void state_
   const int col = lane & 15, grp = lane >> 4;
   const int dv = dv_of(tile, col);  // state column this lane holds
   const int row0 = 32 * w;         // first state row of this wave
-  const int4 si = a.seq_info[n];   // {first chunk, chunks, start, length}
+  const int4 si = seq_info_at(a, n);  // {first chunk, chunks, start, length}
   const int nch = si.y;
   __shared__ Frag<T> xch[2][NW][64];  // S_c fragments, double-buffered by step parity
 

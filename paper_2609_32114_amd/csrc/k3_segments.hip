@@ -486,9 +486,9 @@ __global__ __launch_bounds__(kHeadThreads) void seg_transfer_kernel(PrefillArgs 
   const int pair = item >> 1, part = item & 1;
   if (pair >= a.max_segs * a.Hv) return;  // uniform for the workgroup
   const int s = pair / a.Hv, h = pair % a.Hv;
-  const int4 sg = a.seg_info[s];  // {sequence, first chunk, chunks, index in sequence}
+  const int4 sg = seg_info_at(a, s);  // {sequence, first chunk, chunks, index in sequence}
   if (sg.x < 0) return;
-  if (sg.w == a.seq_seg[sg.x].y - 1) return;  // the last segment's map is never applied
+  if (sg.w == seq_seg_at(a, sg.x).y - 1) return;  // the last segment's map is never applied
   if (part == 0) {
     // the first segment's map acts on the initial state; with none only B_seg is used
     if (sg.w == 0 && !a.s0) return;
@@ -540,14 +540,15 @@ template <typename T, int DK, int DV, bool KDA>
 __global__ __launch_bounds__(kHeadThreads) void seg_state_kernel(PrefillArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   constexpr int CT = DV / 64, RT = DK / 16;
+  single_status(a);
   const int pair = xcd_item(blockIdx.x, 1);
   if (pair >= a.max_segs * a.Hv) return;  // uniform for the workgroup
   const int s = pair / a.Hv, h = pair % a.Hv;
-  const int4 sg = a.seg_info[s];  // {sequence, first chunk, chunks, index in sequence}
+  const int4 sg = seg_info_at(a, s);  // {sequence, first chunk, chunks, index in sequence}
   if (sg.x < 0) return;
   const int n = sg.x;
-  const int4 si = a.seq_info[n];  // {first chunk, chunks, start token, length}
-  const int2 ss = a.seq_seg[n];   // {first segment, segments}
+  const int4 si = seq_info_at(a, n);  // {first chunk, chunks, start token, length}
+  const int2 ss = seq_seg_at(a, n);   // {first segment, segments}
   const int tid = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
