@@ -110,12 +110,12 @@ template <typename T, bool KDA> constexpr int pipe_depth() {
   return sizeof(T) == 2 ? (KDA ? 2 : 3) : 2;
 }
 
-template <typename T, int DK, int DV, bool KDA>
+template <typename T, int DK, int DV, bool KDA, bool SINGLE>
 __global__ __launch_bounds__(64 * (DK / 32), sizeof(T) == 2 ? 2 : 1) void state_prop_kernel(PrefillArgs a) {
   constexpr int NW = DK / 32;   // waves per chain
   constexpr int NT = DV / 16;   // d_v tiles per head
   constexpr int D = pipe_depth<T, KDA>();
-  single_status(a);
+  single_status<SINGLE>(a);
   const int b = blockIdx.x;
   const int xcd = b % kXcds, slot = b / kXcds;
   const int pair = (slot / NT) * kXcds + xcd;
@@ -126,7 +126,7 @@ __global__ __launch_bounds__(64 * (DK / 32), sizeof(T) == 2 ? 2 : 1) void state_
   const int col = lane & 15, grp = lane >> 4;
   const int dv = dv_of(tile, col);  // state column this lane holds
   const int row0 = 32 * w;         // first state row of this wave
-  const int4 si = seq_info_at(a, n);  // {first chunk, chunks, start, length}
+  const int4 si = seq_info_at<SINGLE>(a, n);  // {first chunk, chunks, start, length}
   const int nch = si.y;
   __shared__ Frag<T> xch[2][NW][64];  // S_c fragments, double-buffered by step parity
 
@@ -287,8 +287,12 @@ static hipError_t launch_state_t(const PrefillArgs &a, hipStream_t stream) {
   const long pairs = (long)a.N * a.Hv;
   const long groups = (pairs + kXcds - 1) / kXcds;
   const long blocks = groups * kXcds * (DV / 16);
-  hipLaunchKernelGGL((state_prop_kernel<T, DK, DV, KDA>), dim3((unsigned)blocks), dim3(64 * (DK / 32)), 0, stream,
-                     a);
+  if (a.single)
+    hipLaunchKernelGGL((state_prop_kernel<T, DK, DV, KDA, true>), dim3((unsigned)blocks), dim3(64 * (DK / 32)), 0,
+                       stream, a);
+  else
+    hipLaunchKernelGGL((state_prop_kernel<T, DK, DV, KDA, false>), dim3((unsigned)blocks), dim3(64 * (DK / 32)), 0,
+                       stream, a);
   return hipGetLastError();
 }
 

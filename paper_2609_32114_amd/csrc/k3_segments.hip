@@ -479,16 +479,16 @@ __device__ __forceinline__ void transfer_part(const PrefillArgs &a, int s, int h
   }
 }
 
-template <typename T, int DK, int DV, bool KDA>
+template <typename T, int DK, int DV, bool KDA, bool SINGLE>
 __global__ __launch_bounds__(kHeadThreads) void seg_transfer_kernel(PrefillArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int item = xcd_item(blockIdx.x, 2);  // (segment, head) x 2 parts
   const int pair = item >> 1, part = item & 1;
   if (pair >= a.max_segs * a.Hv) return;  // uniform for the workgroup
   const int s = pair / a.Hv, h = pair % a.Hv;
-  const int4 sg = seg_info_at(a, s);  // {sequence, first chunk, chunks, index in sequence}
+  const int4 sg = seg_info_at<SINGLE>(a, s);  // {sequence, first chunk, chunks, index in sequence}
   if (sg.x < 0) return;
-  if (sg.w == seq_seg_at(a, sg.x).y - 1) return;  // the last segment's map is never applied
+  if (sg.w == seq_seg_at<SINGLE>(a, sg.x).y - 1) return;  // the last segment's map is never applied
   if (part == 0) {
     // the first segment's map acts on the initial state; with none only B_seg is used
     if (sg.w == 0 && !a.s0) return;
@@ -536,19 +536,19 @@ __device__ __forceinline__ void apply_maps(HeadState<T, DK, DV> &hs, const Prefi
   __syncthreads();  // the stage memory is reused by the walk
 }
 
-template <typename T, int DK, int DV, bool KDA>
+template <typename T, int DK, int DV, bool KDA, bool SINGLE>
 __global__ __launch_bounds__(kHeadThreads) void seg_state_kernel(PrefillArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   constexpr int CT = DV / 64, RT = DK / 16;
-  single_status(a);
+  single_status<SINGLE>(a);
   const int pair = xcd_item(blockIdx.x, 1);
   if (pair >= a.max_segs * a.Hv) return;  // uniform for the workgroup
   const int s = pair / a.Hv, h = pair % a.Hv;
-  const int4 sg = seg_info_at(a, s);  // {sequence, first chunk, chunks, index in sequence}
+  const int4 sg = seg_info_at<SINGLE>(a, s);  // {sequence, first chunk, chunks, index in sequence}
   if (sg.x < 0) return;
   const int n = sg.x;
-  const int4 si = seq_info_at(a, n);  // {first chunk, chunks, start token, length}
-  const int2 ss = seq_seg_at(a, n);   // {first segment, segments}
+  const int4 si = seq_info_at<SINGLE>(a, n);  // {first chunk, chunks, start token, length}
+  const int2 ss = seq_seg_at<SINGLE>(a, n);   // {first segment, segments}
   const int tid = threadIdx.x;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
@@ -641,7 +641,7 @@ static long xcd_blocks(const PrefillArgs &a, int per_item) {
 template <typename T, int DK, int DV, bool KDA>
 static hipError_t launch_transfer_t(const PrefillArgs &a, hipStream_t stream) {
   const size_t lds = transfer_lds<T, DK, DV>();
-  auto kern = seg_transfer_kernel<T, DK, DV, KDA>;
+  auto kern = a.single ? seg_transfer_kernel<T, DK, DV, KDA, true> : seg_transfer_kernel<T, DK, DV, KDA, false>;
   hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3((unsigned)xcd_blocks(a, 2)), dim3(kHeadThreads), lds, stream, a);
@@ -651,7 +651,7 @@ static hipError_t launch_transfer_t(const PrefillArgs &a, hipStream_t stream) {
 template <typename T, int DK, int DV, bool KDA>
 static hipError_t launch_state_t(const PrefillArgs &a, hipStream_t stream) {
   const size_t lds = state_lds<T, DK, DV>();
-  auto kern = seg_state_kernel<T, DK, DV, KDA>;
+  auto kern = a.single ? seg_state_kernel<T, DK, DV, KDA, true> : seg_state_kernel<T, DK, DV, KDA, false>;
   hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3((unsigned)xcd_blocks(a, 1)), dim3(kHeadThreads), lds, stream, a);

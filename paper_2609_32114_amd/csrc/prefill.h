@@ -78,44 +78,54 @@ struct PrefillArgs {
   int single;
 };
 
-// The tables of the chunk index kernel, or for a single sequence the same
-// entries derived in place.  A single sequence's cu_seqlens must be {0, T};
-// otherwise it has no chunks (nothing is written to o and its final state is
-// the initial one) and the state kernels report HAGDN_DEV_BAD_SEQLENS.
+// The tables of the chunk index kernel, or for a single sequence (SINGLE:
+// the kernels' separate instances for N = 1) the same entries derived in
+// place.  A single sequence's cu_seqlens must be {0, T}; otherwise it has no
+// chunks (nothing is written to o and its final state is the initial one)
+// and the state kernels report HAGDN_DEV_BAD_SEQLENS.
 __device__ __forceinline__ bool single_ok(const PrefillArgs &a) {
   return a.cu_seqlens[0] == 0 && a.cu_seqlens[1] == a.T;
 }
 // {first chunk, chunks, start token, length} of sequence n
+template <bool SINGLE>
 __device__ __forceinline__ int4 seq_info_at(const PrefillArgs &a, int n) {
-  if (a.single) {
+  if constexpr (SINGLE) {
     const bool ok = single_ok(a);
     return make_int4(0, ok ? (a.T + kChunk - 1) / kChunk : 0, 0, ok ? a.T : 0);
+  } else {
+    return a.seq_info[n];
   }
-  return a.seq_info[n];
 }
 // {first segment, segments} of sequence n
+template <bool SINGLE>
 __device__ __forceinline__ int2 seq_seg_at(const PrefillArgs &a, int n) {
-  if (a.single) {
-    const int nch = seq_info_at(a, 0).y;
+  if constexpr (SINGLE) {
+    const int nch = seq_info_at<true>(a, 0).y;
     return make_int2(0, nch > 0 ? (nch + a.seg_chunks - 1) / a.seg_chunks : 1);
+  } else {
+    return a.seq_seg[n];
   }
-  return a.seq_seg[n];
 }
 // {sequence (-1 = unused), first chunk, chunks, index in sequence} of segment s
+template <bool SINGLE>
 __device__ __forceinline__ int4 seg_info_at(const PrefillArgs &a, int s) {
-  if (a.single) {
-    const int nch = seq_info_at(a, 0).y;
+  if constexpr (SINGLE) {
+    const int nch = seq_info_at<true>(a, 0).y;
     const int nseg = nch > 0 ? (nch + a.seg_chunks - 1) / a.seg_chunks : 1;
     if (s >= nseg) return make_int4(-1, 0, 0, 0);
     const int c0 = s * a.seg_chunks;
     return make_int4(0, c0, min(a.seg_chunks, nch - c0), s);
+  } else {
+    return a.seg_info[s];
   }
-  return a.seg_info[s];
 }
 // The device status word, written by one thread of the state kernel when the
 // chunk index kernel did not run (a single sequence).
+template <bool SINGLE>
 __device__ __forceinline__ void single_status(const PrefillArgs &a) {
-  if (a.single && blockIdx.x == 0 && threadIdx.x == 0) a.status[0] = single_ok(a) ? 0 : 1;
+  if constexpr (SINGLE) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) a.status[0] = single_ok(a) ? 0 : 1;
+  }
 }
 
 // One decode step: a single token for each of N sequences whose states live
