@@ -2,8 +2,10 @@
 // (paper Sec. 2.1, operator #5 H), the only step that is sequential over
 // chunks, fused with the final Map (operator #6 O), for chains walked whole.
 // One workgroup per (sequence, value head, 16-column tile of d_v); the tile's
-// columns are dv_of(tile, 0..15) (device.h).  Chains long enough to pay for
-// segment maps take the segment-parallel path of k3_segments.hip instead.
+// columns are dv_of(tile, 0..15) (device.h).  Batches with more walks than
+// CUs use a second instance that walks two adjacent tiles per workgroup
+// (state_prop2_kernel, below).  Chains long enough to pay for segment maps
+// take the segment-parallel path of k3_segments.hip instead.
 //
 // Per chunk the chunk-local kernel has reduced operator #5 to an affine map of
 // the state entering the chunk (S^T, d_k x d_v):
