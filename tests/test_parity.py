@@ -184,8 +184,8 @@ def test_workload2_shape_stress(variant):
     check_against_oracle(inp, heads=[4], label=f"workload2-{variant}")
 
 
-# More walk workgroups than CUs (N x Hv x Dv/16 > 256): walks share CUs (two
-# per CU for bf16) and the later ones start only when earlier ones finish.
+# More walk workgroups than CUs (N x Hv x Dv/16 > 256): bf16 walks pair
+# adjacent tiles in one workgroup, and walks share CUs.
 # Long-memory gates so that the state carries across every chunk; the oracle
 # checks every head.
 MANY_WALKS = [
@@ -195,6 +195,9 @@ MANY_WALKS = [
     ("gdn", (130, 0, 260, 64, 1), 4, 16, 64, 64),
     ("kda", (200, 129), 2, 40, 128, 64),
     ("gdn", (129, 200), 8, 40, 64, 128),
+    # a single sequence with more walks than CUs (its own kernel instances)
+    ("gdn", (700,), 8, 48, 128, 128),
+    ("kda", (300,), 4, 40, 128, 128),
 ]
 
 
