@@ -207,10 +207,11 @@ int hagdn_version(void);
  * parallel, then each segment walks its own chunks from the state the earlier
  * segments' maps give.  Results are the same for every L up to rounding
  * order.  hagdn_set_segment_chunks(0) restores the automatic choice (a
- * function of N, T_total, Hv and Dv); a positive value forces L for every later call in the
- * process (both capped; see hagdn_segment_chunks).  Not synchronised with
- * calls in flight on other host threads: set it before querying workspace
- * sizes.  Returns HAGDN_OK or HAGDN_EINVAL (chunks < 0 or > 2^20). */
+ * function of N, T_total, Hv and Dv); a positive value forces L for every
+ * later call in the process (both capped; see hagdn_segment_chunks).  Not
+ * synchronised with calls in flight on other host threads: set it before
+ * querying workspace sizes.  Returns HAGDN_OK or HAGDN_EINVAL (chunks < 0 or
+ * > 2^20). */
 int hagdn_set_segment_chunks(int chunks);
 
 /* L that a call with these sizes and dtype would use now; -1 on invalid
