@@ -126,11 +126,18 @@ __device__ __forceinline__ void gam8(const float *g, int r, int d, float (&x)[8]
 struct LocalItem {
   int c, h, start, len;  // len 0: past the last chunk
 };
-__device__ __forceinline__ LocalItem local_item(const PrefillArgs &a, int item) {
+// Workgroup b -> item: the value heads of one q/k group (grouped heads share
+// q and k) take consecutive ids of one XCD (ids b, b+8, ... share an XCD and
+// its L2), so all but the first read q and k from L2.  Without grouping this
+// is the identity.  The grid is padded to whole rounds of 8 groups.
+__device__ __forceinline__ LocalItem local_item(const PrefillArgs &a, int b) {
   LocalItem it{0, 0, 0, 0};
-  if (item < a.max_chunks * a.Hv) {
-    it.c = item / a.Hv;
-    it.h = item % a.Hv;
+  const int G = a.Hv / a.Hqk;  // value heads per q/k head
+  const int xcd = b % 8, slot = b / 8;
+  const int grp = (slot / G) * 8 + xcd;  // (chunk, q/k head) group
+  if (grp < a.max_chunks * a.Hqk) {
+    it.c = grp / a.Hqk;
+    it.h = (grp % a.Hqk) * G + slot % G;
     if (a.single) {  // chunk c of the only sequence (tokens [0, T))
       it.start = it.c * kChunk;
       it.len = max(0, min(kChunk, a.T - it.start));
@@ -731,7 +738,9 @@ static hipError_t launch_local_t(const PrefillArgs &a, hipStream_t stream) {
   using L = LocalLayout<T, DK, DV, KDA>;
   hipError_t e = set_lds_limit<T, DK, DV, KDA, PRE>();
   if (e != hipSuccess) return e;
-  const long items = (long)a.max_chunks * a.Hv;  // one workgroup per (chunk, value head) block
+  // one workgroup per (chunk, value head) block, padded to whole rounds of 8 q/k groups
+  const long groups = (long)a.max_chunks * a.Hqk;
+  const long items = (groups + 7) / 8 * 8 * (a.Hv / a.Hqk);
   hipLaunchKernelGGL((chunk_local_kernel<T, DK, DV, KDA, PRE>), dim3((unsigned)items), dim3(kLocalThreads), L::bytes,
                      stream, a);
   return hipGetLastError();
