@@ -50,9 +50,10 @@
  *   the host before anything is enqueued; on a non-OK return nothing was
  *   launched (except HAGDN_EHIP: a launch failed) and hagdn_last_error()
  *   describes the problem.  Contents of cu_seqlens live on the device and are
- *   checked by the first kernel: if they are malformed, no token is processed
- *   (o is left untouched, s_final receives s0 or zeros) and
- *   hagdn_device_status() reports HAGDN_DEV_BAD_SEQLENS afterwards.
+ *   checked on the device (by the first kernel, or for N = 1 by the state
+ *   kernel): if they are malformed, no token is processed (o is left
+ *   untouched, s_final receives s0 or zeros) and hagdn_device_status()
+ *   reports HAGDN_DEV_BAD_SEQLENS afterwards.
  */
 #ifndef HAGDN_H
 #define HAGDN_H
@@ -74,7 +75,8 @@ typedef enum {
 
 typedef enum { HAGDN_F32 = 0, HAGDN_BF16 = 1 } hagdn_dtype;
 
-/* Device-side status word written by the first kernel of every call. */
+/* Device-side status word written by every prefill call (by its first
+ * kernel, or for a single sequence by its state kernel). */
 typedef enum { HAGDN_DEV_OK = 0, HAGDN_DEV_BAD_SEQLENS = 1 } hagdn_device_code;
 
 /* Bytes of device workspace gdn_prefill needs for these sizes (0 if the
