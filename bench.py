@@ -185,7 +185,7 @@ def main():
 
     value = T / (ms * 1e-3)
     dom = max(kernel_ms, key=kernel_ms.get)
-    L = P.segment_chunks(N, T, Hv, Dv, torch.bfloat16 if esz == 2 else torch.float32)
+    L = P.segment_chunks(N, T, Hv, Dv, torch.bfloat16 if esz == 2 else torch.float32, kind=inp.kind)
     dom_bytes = cost.kernel_bytes(dom, T, N, Hqk, Hv, Dk, Dv, esz, kda, inp.s0 is not None,
                                   seg_chunks=L)
     dom_ms = kernel_ms[dom]

@@ -209,20 +209,20 @@ int hagdn_version(void);
  * parallel, then each segment walks its own chunks from the state the earlier
  * segments' maps give.  Results are the same for every L up to rounding
  * order.  hagdn_set_segment_chunks(0) restores the automatic choice (a
- * function of N, T_total, Hv and Dv); a positive value forces L for every
- * later call in the process (both capped; see hagdn_segment_chunks).  Not
- * synchronised with calls in flight on other host threads: set it before
- * querying workspace sizes.  Returns HAGDN_OK or HAGDN_EINVAL (chunks < 0 or
- * > 2^20). */
+ * function of N, T_total, Hv, Dv and the gate kind); a positive value forces
+ * L for every later call in the process (both capped; see
+ * hagdn_segment_chunks).  Not synchronised with calls in flight on other host
+ * threads: set it before querying workspace sizes.  Returns HAGDN_OK or
+ * HAGDN_EINVAL (chunks < 0 or > 2^20). */
 int hagdn_set_segment_chunks(int chunks);
 
-/* L that a call with these sizes and dtype would use now; -1 on invalid
- * sizes or dtype.  Automatic or forced, L is capped at the largest value with
- * 64 L Hv Dv elements of dtype below 2 GiB, so the output rows of one segment
- * stay addressable with 32-bit byte offsets; the cap depends on Hv, Dv and
- * dtype, never on T_total.  A call whose sequences can be longer than L chunks
- * takes the segmented path. */
-int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv, int dtype);
+/* L that a call with these sizes and dtype would use now (kda: 0 for
+ * gdn_prefill, 1 for kda_prefill); -1 on invalid sizes or dtype.  Automatic or
+ * forced, L is capped at the largest value with 64 L Hv Dv elements of dtype
+ * below 2 GiB, so the output rows of one segment stay addressable with 32-bit
+ * byte offsets; the cap depends on Hv, Dv and dtype, never on T_total.  A
+ * call whose sequences can be longer than L chunks takes the segmented path. */
+int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv, int dtype, int kda);
 
 #ifdef __cplusplus
 }

@@ -65,7 +65,7 @@ _SYMBOLS = {
     "hagdn_kernel_name": (ctypes.c_char_p, [ctypes.c_int]),
     "hagdn_version": (ctypes.c_int, []),
     "hagdn_set_segment_chunks": (ctypes.c_int, [ctypes.c_int]),
-    "hagdn_segment_chunks": (ctypes.c_int, [ctypes.c_int] * 5),
+    "hagdn_segment_chunks": (ctypes.c_int, [ctypes.c_int] * 6),
 }
 
 
@@ -265,13 +265,16 @@ def set_segment_chunks(chunks: int):
         raise HagdnError(rc, _err(lib))
 
 
-def segment_chunks(N: int, T: int, Hv: int, Dv: int, dtype=None) -> int:
-    """Segment length a call with these sizes and I/O dtype (torch.bfloat16,
-    the default, or torch.float32) would use now."""
+def segment_chunks(N: int, T: int, Hv: int, Dv: int, dtype=None, kind: str = "gdn") -> int:
+    """Segment length a gdn_prefill (kind "gdn") or kda_prefill ("kda") call
+    with these sizes and I/O dtype (torch.bfloat16, the default, or
+    torch.float32) would use now."""
     import torch
     lib = load_library()
     code = _dtype_code(torch.bfloat16 if dtype is None else dtype)
-    L = lib.hagdn_segment_chunks(int(N), int(T), int(Hv), int(Dv), code)
+    if kind not in ("gdn", "kda"):
+        raise ValueError(f"kind must be 'gdn' or 'kda', not {kind!r}")
+    L = lib.hagdn_segment_chunks(int(N), int(T), int(Hv), int(Dv), code, int(kind == "kda"))
     if L < 0:
         raise HagdnError(1, _err(lib))
     return L

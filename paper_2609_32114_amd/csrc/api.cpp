@@ -68,13 +68,18 @@ constexpr long kCus = 256;  // compute units of an MI355X (gfx950)
 // one segment workgroup on every CU (L = n Hv / 256, at least 12).  With 32
 // heads (256 walk workgroups) the whole walk still won at 256 chunks (604 us
 // against 682), so the threshold grows with the walks' share of the CUs.
+// KDA pays from fewer chunks: its per-channel gate adds 8 KiB per token
+// (d = 128) to the chunk-local kernel's input and pushes the walk's operands
+// out of the Infinity Cache sooner.  With 16 heads: T = 6144 185 us whole
+// against 186 at L = 12; T = 8192 249 against 230 at L = 8; T = 12288 395
+// against 331 at L = 12.  KDA segments from 112 chunks with L at least 8.
 //
 // Whatever the choice (or override), L is capped so that the o rows of one
 // segment, 64 L Hv Dv elements, span less than 2 GiB: the walk kernels address
 // a segment's rows through one buffer resource with 32-bit signed byte
 // offsets.  A call whose chains do not fit one capped segment takes the
 // segmented path, whose windows then fit too.
-int seg_chunks(int N, int T, int Hv, int Dv, size_t esz) {
+int seg_chunks(int N, int T, int Hv, int Dv, size_t esz, bool kda) {
   const size_t seg_rows_bytes = (size_t)hagdn::kChunk * (size_t)Hv * (size_t)Dv * esz;
   const long cap = std::max<long>(1, (long)(((size_t)1 << 31) - 1) / (long)seg_rows_bytes);
   const int ov = g_seg_override.load(std::memory_order_relaxed);
@@ -85,9 +90,9 @@ int seg_chunks(int N, int T, int Hv, int Dv, size_t esz) {
     const long n_all = ((long)T + hagdn::kChunk - 1) / hagdn::kChunk;  // longest possible chain
     const long n_avg = ((long)T / (N > 0 ? N : 1) + hagdn::kChunk - 1) / hagdn::kChunk;
     const double walks = (double)(N > 0 ? N : 1) * Hv * std::max(1, Dv / 16);
-    const double threshold = 144.0 * std::max(1.0, walks / (kCus / 2));
+    const double threshold = (kda ? 112.0 : 144.0) * std::max(1.0, walks / (kCus / 2));
     if ((double)n_avg < threshold) L = n_all > 0 ? std::min<long>(n_all, kMaxSegChunks) : 1;
-    else L = std::max<long>(12, (n_all * Hv + kCus - 1) / kCus);
+    else L = std::max<long>(kda ? 8 : 12, (n_all * Hv + kCus - 1) / kCus);
   }
   return (int)std::min(L, cap);
 }
@@ -102,14 +107,14 @@ struct Layout {
 };
 
 // Returns false (with the error set) if the sizes overflow.
-bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, Layout *L) {
+bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, bool kda, Layout *L) {
   const size_t mc = (size_t)(T / hagdn::kChunk) + (size_t)N;
   if (mc > 0x7fffffffu) {
     fail(HAGDN_EINVAL, "too many chunks (%zu)", mc);
     return false;
   }
   L->max_chunks = (int)mc;
-  L->seg_chunks = seg_chunks(N, T, Hv, Dv, esz);
+  L->seg_chunks = seg_chunks(N, T, Hv, Dv, esz, kda);
   const size_t ms = mc / (size_t)L->seg_chunks + (size_t)N;
   L->max_segs = (int)ms;  // <= mc
   size_t blocks, sblocks;  // (chunk, value head) and (segment, value head) blocks
@@ -159,10 +164,10 @@ int check_shapes(int N, int T, int Hqk, int Hv, int Dk, int Dv, int dtype) {
   return HAGDN_OK;
 }
 
-size_t workspace_size(int N, int T, int Hqk, int Hv, int Dk, int Dv, int dtype) {
+size_t workspace_size(bool kda, int N, int T, int Hqk, int Hv, int Dk, int Dv, int dtype) {
   if (check_shapes(N, T, Hqk, Hv, Dk, Dv, dtype) != HAGDN_OK) return 0;
   Layout L;
-  if (!make_layout(N, T, Hv, Dk, Dv, dtype == HAGDN_BF16 ? 2 : 4, &L)) return 0;
+  if (!make_layout(N, T, Hv, Dk, Dv, dtype == HAGDN_BF16 ? 2 : 4, kda, &L)) return 0;
   return L.total;
 }
 
@@ -211,7 +216,7 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   }
   const bool bf16 = dtype == HAGDN_BF16;
   Layout L;
-  if (!make_layout(N, T, Hv, Dk, Dv, bf16 ? 2 : 4, &L)) return HAGDN_EINVAL;
+  if (!make_layout(N, T, Hv, Dk, Dv, bf16 ? 2 : 4, kda, &L)) return HAGDN_EINVAL;
   if (ws_bytes < L.total)
     return fail(HAGDN_EWORKSPACE, "workspace too small: %zu bytes given, %zu needed", ws_bytes, L.total);
 
@@ -317,11 +322,11 @@ int decode(bool kda, const void *q, const void *k, const void *v, const float *g
 extern "C" {
 
 size_t gdn_prefill_workspace_size(int N, int T_total, int Hqk, int Hv, int Dk, int Dv, int dtype) {
-  return workspace_size(N, T_total, Hqk, Hv, Dk, Dv, dtype);
+  return workspace_size(false, N, T_total, Hqk, Hv, Dk, Dv, dtype);
 }
 
 size_t kda_prefill_workspace_size(int N, int T_total, int Hqk, int Hv, int Dk, int Dv, int dtype) {
-  return workspace_size(N, T_total, Hqk, Hv, Dk, Dv, dtype);
+  return workspace_size(true, N, T_total, Hqk, Hv, Dk, Dv, dtype);
 }
 
 int gdn_prefill(const void *q, const void *k, const void *v, const float *g, const float *beta,
@@ -448,11 +453,11 @@ int hagdn_set_segment_chunks(int chunks) {
   return HAGDN_OK;
 }
 
-int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv, int dtype) {
+int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv, int dtype, int kda) {
   if (N < 1 || T_total < 0 || Hv < 1 || Dv < 1)
     return fail(HAGDN_EINVAL, "bad shape"), -1;
   if (dtype != HAGDN_F32 && dtype != HAGDN_BF16) return fail(HAGDN_EINVAL, "bad dtype %d", dtype), -1;
-  return seg_chunks(N, T_total, Hv, Dv, dtype == HAGDN_BF16 ? 2 : 4);
+  return seg_chunks(N, T_total, Hv, Dv, dtype == HAGDN_BF16 ? 2 : 4, kda != 0);
 }
 
 }  // extern "C"

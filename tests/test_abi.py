@@ -116,6 +116,14 @@ def test_segment_length_knob():
         assert P.segment_chunks(1, 16384, 32, 128) == 256   # 256 walk workgroups: threshold 288
         assert P.segment_chunks(1, 18432, 32, 128) == 36    # 288 chunks: 288 x 32 / 256
         assert P.segment_chunks(8, 34816, 32, 128) == 544   # short average chains: whole
+        # KDA segments from 112 chunks, L at least 8
+        assert P.segment_chunks(1, 7104, 16, 128, kind="kda") == 111
+        assert P.segment_chunks(1, 7168, 16, 128, kind="kda") == 8
+        assert P.segment_chunks(1, 8192, 16, 128, kind="kda") == 8
+        assert P.segment_chunks(1, 12288, 16, 128, kind="kda") == 12
+        assert P.segment_chunks(1, 8192, 16, 128, kind="gdn") == 128
+        with pytest.raises(ValueError):
+            P.segment_chunks(1, 8192, 16, 128, kind="mamba")
         P.set_segment_chunks(8)
         auto = P.segment_chunks(1, 4096, 16, 128)
         assert auto == 8
