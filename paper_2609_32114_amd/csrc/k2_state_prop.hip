@@ -2,10 +2,10 @@
 // (paper Sec. 2.1, operator #5 H), the only step that is sequential over
 // chunks, fused with the final Map (operator #6 O), for chains walked whole.
 // One workgroup per (sequence, value head, 16-column tile of d_v); the tile's
-// columns are dv_of(tile, 0..15) (device.h).  Batches with more walks than
-// CUs use a second instance that walks two adjacent tiles per workgroup
-// (state_prop2_kernel, below).  Chains long enough to pay for segment maps
-// take the segment-parallel path of k3_segments.hip instead.
+// columns are dv_of(tile, 0..15) (device.h).  bf16 batches with more walks
+// than CUs take the staged walk of k2_walk.hip, which shares a chunk's
+// operands among several tiles of a head.  Chains long enough to pay for
+// segment maps take the segment-parallel path of k3_segments.hip instead.
 //
 // Per chunk the chunk-local kernel has reduced operator #5 to an affine map of
 // the state entering the chunk (S^T, d_k x d_v):
@@ -286,205 +286,6 @@ __global__ __launch_bounds__(64 * (DK / 32), sizeof(T) == 2 ? 2 : 1) void state_
   }
 }
 
-// Paired-tile walk (bf16, more walks than CUs): one workgroup walks two
-// adjacent 16-column tiles of a head.  Both tiles need the same NM rows, Q'
-// block and decay, so a pair moves 60 KiB per step where two single-tile
-// walks move 108 KiB, and the step's matrix work doubles behind the same
-// exchange and barrier.  Throughput-bound batches have the CUs to spare.
-template <typename T, int DK, bool KDA>
-struct StepOps2 {
-  Frag<T> nm[2][DK / 32];         // NM rows 32w + 16i + col, k-block kb (both tiles)
-  typename Raw4<T>::type b[2][2]; // B[32w + 16i + 4grp .. +3][dv of tile t]
-  f32x4 dec[2];                   // decay of the rows (GDN: dec[0][0] only)
-};
-template <typename T, int DK>
-struct OutOps2 {
-  static constexpr int TPW = 4 / (DK / 32);
-  Frag<T> qp[TPW][DK / 32];          // Q' block (token tile, kb), both tiles
-  typename Raw4<T>::type ol[2][TPW]; // O_loc block (tile t, token tile)
-};
-template <typename T, bool KDA> constexpr int pipe_depth2() { return KDA ? 2 : 2; }
-
-template <typename T, int DK, int DV, bool KDA, bool SINGLE>
-__global__ __launch_bounds__(64 * (DK / 32), 2) void state_prop2_kernel(PrefillArgs a) {
-  constexpr int NW = DK / 32;   // waves per chain
-  constexpr int NP = DV / 32;   // tile pairs per head
-  constexpr int D = pipe_depth2<T, KDA>();
-  single_status<SINGLE>(a);
-  const int b = blockIdx.x;
-  const int xcd = b % kXcds, slot = b / kXcds;
-  const int pair = (slot / NP) * kXcds + xcd;
-  const int tp = slot % NP;
-  if (pair >= a.N * a.Hv) return;  // uniform for the workgroup
-  const int n = pair / a.Hv, h = pair % a.Hv;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int col = lane & 15, grp = lane >> 4;
-  int dvt[2];  // state column this lane holds in tile 2tp + t
-#pragma unroll
-  for (int t = 0; t < 2; ++t) dvt[t] = dv_of(2 * tp + t, col);
-  const int row0 = 32 * w;
-  const int4 si = seq_info_at<SINGLE>(a, n);
-  const int nch = si.y;
-  __shared__ Frag<T> xch[2][NW][2][64];  // S_c fragments (wave, tile), double-buffered by step parity
-
-  f32x4 H[2][2];  // H[t][i][e] = S^T[row0 + 16i + 4grp + e][dvt[t]]
-  const size_t sbase = ((size_t)n * a.Hv + h) * DK * DV;
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        H[t][i][e] = a.s0 ? a.s0[sbase + (size_t)(row0 + 16 * i + 4 * grp + e) * DV + dvt[t]] : 0.f;
-
-  if (nch > 0) {
-    const T *__restrict__ NMg = static_cast<const T *>(a.NM);
-    const T *__restrict__ Bg = static_cast<const T *>(a.Bc);
-    const float *__restrict__ decg = a.dec;
-    const T *__restrict__ Qpg = static_cast<const T *>(a.Qp);
-    const T *__restrict__ Olg = static_cast<const T *>(a.Ol);
-    const __amdgpu_buffer_rsrc_t orsrc = walk_buffer(static_cast<T *>(a.o) + (size_t)si.z * a.Hv * DV,
-                                                     (uint32_t)((size_t)si.w * a.Hv * DV * sizeof(T)));
-    auto blk = [&](int c) { return (size_t)(si.x + min(c, nch - 1)) * a.Hv + h; };
-    auto nm_at = [&](size_t b, int i, int kb) {
-      return NMg + b * ((size_t)DK * DK) + ((size_t)((2 * w + i) * (DK / 32) + kb) * 64 + lane) * 8;
-    };
-    auto b_at = [&](size_t b, int t, int i) {
-      return Bg + b * ((size_t)DV * DK) + ((size_t)((2 * tp + t) * 64 + lane) * (DK / 16) + 2 * w + i) * 4;
-    };
-    auto qp_at = [&](size_t b, int u, int kb) {
-      return Qpg + b * ((size_t)kChunk * DK) + ((size_t)((w + NW * u) * (DK / 32) + kb) * 64 + lane) * 8;
-    };
-    auto ol_at = [&](size_t b, int t, int u) {
-      return Olg + b * ((size_t)kChunk * DV) + ((size_t)((2 * tp + t) * 64 + lane) * 4 + w + NW * u) * 4;
-    };
-    auto load_dec = [&](StepOps2<T, DK, KDA> &op, size_t b) {
-      if constexpr (KDA) {
-#pragma unroll
-        for (int i = 0; i < 2; ++i) op.dec[i] = load4(decg + b * DK + row0 + 16 * i + 4 * grp);
-      } else {
-        op.dec[0][0] = decg[b * DK];
-      }
-    };
-    auto load = [&](StepOps2<T, DK, KDA> &op, int c) {
-      const size_t b = blk(c);
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-#pragma unroll
-        for (int kb = 0; kb < DK / 32; ++kb) op.nm[i][kb] = load_frag_at(nm_at(b, i, kb));
-#pragma unroll
-        for (int t = 0; t < 2; ++t) op.b[t][i] = load_raw4(b_at(b, t, i));
-      }
-      load_dec(op, b);
-    };
-    constexpr int TPW = OutOps2<T, DK>::TPW;
-    auto load_out = [&](OutOps2<T, DK> &oq, int c) {
-      const size_t b = blk(c);
-#pragma unroll
-      for (int u = 0; u < TPW; ++u) {
-#pragma unroll
-        for (int kb = 0; kb < DK / 32; ++kb) oq.qp[u][kb] = load_frag_at(qp_at(b, u, kb));
-#pragma unroll
-        for (int t = 0; t < 2; ++t) oq.ol[t][u] = load_raw4(ol_at(b, t, u));
-      }
-    };
-    f32x4 pend[2][TPW];
-    auto store_out = [&](int c) {
-      const int base = c * kChunk;  // first token of chunk c inside the sequence
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int u = 0; u < TPW; ++u) {
-          const int r = base + 16 * (w + NW * u) + col;
-          walk_store4(orsrc, (int)(((size_t)r * a.Hv + h) * DV + dv_of(2 * tp + t, 4 * grp)) * (int)sizeof(T), T{},
-                      pend[t][u] * a.scale);
-        }
-    };
-    auto step = [&](StepOps2<T, DK, KDA> &op, OutOps2<T, DK> &oq, int c) {
-      const size_t bn = blk(c + D);
-#pragma unroll
-      for (int t = 0; t < 2; ++t) xch[c & 1][w][t][lane] = frag_from_acc<T>(H[t][0], H[t][1]);
-      __syncthreads();
-      Frag<T> hb[2][NW];
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int kb = 0; kb < NW; ++kb) hb[t][kb] = xch[c & 1][kb][t][lane];
-      store_out(c - 1);  // chunk -1: every row falls outside the buffer range
-      f32x4 acc0[2][2], acc1[2][2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const f32x4 d = KDA ? op.dec[i] : f32x4{op.dec[0][0], op.dec[0][0], op.dec[0][0], op.dec[0][0]};
-          acc0[t][i] = d * H[t][i] + raw4_to_f32(op.b[t][i]);
-          acc1[t][i] = zero4();
-        }
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) op.b[t][i] = load_raw4(b_at(bn, t, i));
-      load_dec(op, bn);
-#pragma unroll
-      for (int kb = 0; kb < NW; ++kb)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-#pragma unroll
-          for (int t = 0; t < 2; ++t) {
-            if (kb & 1) acc1[t][i] = mma(acc1[t][i], op.nm[i][kb], hb[t][kb]);
-            else acc0[t][i] = mma(acc0[t][i], op.nm[i][kb], hb[t][kb]);
-          }
-          op.nm[i][kb] = load_frag_at(nm_at(bn, i, kb));
-        }
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int i = 0; i < 2; ++i) H[t][i] = acc0[t][i] + acc1[t][i];
-#pragma unroll
-      for (int u = 0; u < TPW; ++u) {
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          pend[t][u] = raw4_to_f32(oq.ol[t][u]);
-          oq.ol[t][u] = load_raw4(ol_at(bn, t, u));
-        }
-#pragma unroll
-        for (int kb = 0; kb < NW; ++kb) {
-#pragma unroll
-          for (int t = 0; t < 2; ++t) pend[t][u] = mma(pend[t][u], hb[t][kb], oq.qp[u][kb]);
-          oq.qp[u][kb] = load_frag_at(qp_at(bn, u, kb));
-        }
-      }
-    };
-
-    StepOps2<T, DK, KDA> R[D];
-    OutOps2<T, DK> Q[D];
-#pragma unroll
-    for (int u = 0; u < D; ++u) {
-      load(R[u], u);
-      load_out(Q[u], u);
-    }
-    int c0 = 0;
-    for (; c0 + D <= nch; c0 += D) {
-#pragma unroll
-      for (int u = 0; u < D; ++u) step(R[u], Q[u], c0 + u);
-    }
-#pragma unroll
-    for (int u = 0; u < D; ++u)
-      if (c0 + u < nch) step(R[u], Q[u], c0 + u);  // uniform for the workgroup
-    store_out(nch - 1);
-  }
-
-  if (a.s_final) {
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          a.s_final[sbase + (size_t)(row0 + 16 * i + 4 * grp + e) * DV + dvt[t]] = H[t][i][e];
-  }
-}
-
 // CUs of the current device, looked up once per device.
 static hipError_t device_cus(int *out) {
   constexpr int kMaxDevices = 64;
@@ -506,22 +307,6 @@ static hipError_t launch_state_t(const PrefillArgs &a, hipStream_t stream) {
   const long pairs = (long)a.N * a.Hv;
   const long groups = (pairs + kXcds - 1) / kXcds;
   const long blocks = groups * kXcds * (DV / 16);
-  if constexpr (sizeof(T) == 2) {
-    // more walks than CUs: pair the tiles (the single-tile walk would queue)
-    int cus = 0;
-    hipError_t e = device_cus(&cus);
-    if (e != hipSuccess) return e;
-    if (blocks > cus) {
-      const long blocks2 = groups * kXcds * (DV / 32);
-      if (a.single)
-        hipLaunchKernelGGL((state_prop2_kernel<T, DK, DV, KDA, true>), dim3((unsigned)blocks2), dim3(64 * (DK / 32)),
-                           0, stream, a);
-      else
-        hipLaunchKernelGGL((state_prop2_kernel<T, DK, DV, KDA, false>), dim3((unsigned)blocks2),
-                           dim3(64 * (DK / 32)), 0, stream, a);
-      return hipGetLastError();
-    }
-  }
   if (a.single)
     hipLaunchKernelGGL((state_prop_kernel<T, DK, DV, KDA, true>), dim3((unsigned)blocks), dim3(64 * (DK / 32)), 0,
                        stream, a);
@@ -540,7 +325,15 @@ static hipError_t dispatch_dims(const PrefillArgs &a, hipStream_t s) {
 }
 
 hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStream_t s) {
-  if (bf16) return kda ? dispatch_dims<bf16_t, true>(a, s) : dispatch_dims<bf16_t, false>(a, s);
+  if (bf16) {
+    // more walks than CUs: the staged walk, several tiles per workgroup
+    int cus = 0;
+    hipError_t e = device_cus(&cus);
+    if (e != hipSuccess) return e;
+    const long walks = ((long)a.N * a.Hv + kXcds - 1) / kXcds * kXcds * (a.Dv / 16);
+    if (walks > cus) return launch_state_walk(a, kda, cus, s);
+    return kda ? dispatch_dims<bf16_t, true>(a, s) : dispatch_dims<bf16_t, false>(a, s);
+  }
   return kda ? dispatch_dims<float, true>(a, s) : dispatch_dims<float, false>(a, s);
 }
 

@@ -198,6 +198,10 @@ MANY_WALKS = [
     # a single sequence with more walks than CUs (its own kernel instances)
     ("gdn", (700,), 8, 48, 128, 128),
     ("kda", (300,), 4, 40, 128, 128),
+    # more than twice as many walks as CUs: four tiles per walk workgroup
+    ("kda", (130, 70, 200, 65), 8, 40, 128, 128),
+    ("gdn", (300,), 8, 96, 128, 128),
+    ("gdn", (100, 37), 4, 80, 64, 64),
 ]
 
 
