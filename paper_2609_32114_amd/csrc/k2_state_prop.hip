@@ -106,10 +106,10 @@ struct OutOps {
 
 // Chunks of operands in flight: 3 for bf16 GDN, 2 for bf16 KDA (wider decay
 // operands) and for fp32.  The bf16 depths fit the operand ring in 256
-// architectural registers with no accumulation registers, so two walks can
-// share a CU.  A deeper ring (4 chunks) measured slower even for one walk per
-// CU: it spills into accumulation registers, and the copies back land on the
-// chain (workload of 1 x 4096 tokens, 16 heads: 53.2 against 51.3 us).
+// architectural registers with no accumulation registers.  A deeper ring (4
+// chunks) measured slower: it spills into accumulation registers, and the
+// copies back land on the chain (workload of 1 x 4096 tokens, 16 heads: 53.2
+// against 51.3 us).
 template <typename T, bool KDA> constexpr int pipe_depth() {
   return sizeof(T) == 2 ? (KDA ? 2 : 3) : 2;
 }

@@ -202,6 +202,8 @@ MANY_WALKS = [
     ("kda", (130, 70, 200, 65), 8, 40, 128, 128),
     ("gdn", (300,), 8, 96, 128, 128),
     ("gdn", (100, 37), 4, 80, 64, 64),
+    ("kda", (90, 40), 4, 96, 64, 64),
+    ("kda", (150,), 2, 40, 64, 128),
 ]
 
 
