@@ -59,10 +59,10 @@ __device__ __forceinline__ void walk_store4(__amdgpu_buffer_rsrc_t r, int off, f
 // S_c as bf16 B fragments -> o of chunk c-1 stored -> S <- D S + B ->
 // for each k-block: S += NM(:, kb) S_c(kb) and O^T += S_c(kb) Q'(:, kb)^T,
 // the LDS operand reads running one k-block ahead of the products.
-template <typename T, int DK, bool KDA>
+template <typename T, int DK, bool KDA, bool QP = true>
 struct WalkStage {
   static constexpr int NM_BYTES = DK * DK * (int)sizeof(T);
-  static constexpr int QP_BYTES = kChunk * DK * (int)sizeof(T);
+  static constexpr int QP_BYTES = QP ? kChunk * DK * (int)sizeof(T) : 0;
   static constexpr int DEC_BYTES = KDA ? DK * 4 : 0;
   static constexpr int NM_OPS = NM_BYTES / 1024, QP_OPS = QP_BYTES / 1024;  // 16-byte lane loads
   static constexpr int DEC_OPS = DEC_BYTES / 256;                            // 4-byte lane loads
@@ -276,6 +276,234 @@ __global__ __launch_bounds__(64 * (TPW + 1), 1) void state_walk_kernel(PrefillAr
 }
 
 
+// ---------------------------------------------------------------------------
+// Segment maps on the staged walk (bf16; the Chunk-Seg-Seg path, paper Sec. 4):
+// the chunk maps of one segment composed, S^T_out = A S^T_in + B_seg.  A is the
+// walk of the d_k x d_k identity through the segment's chunks without their B
+// terms, B_seg the walk of a zero state with them; both are column tiles, so
+// each tile wave walks one 16-column tile of A or of B_seg and a loader wave
+// stages the chunks' NM blocks (shared by every tile) as above.  Workgroups of
+// TPW tiles: d_k / (16 TPW) of them for A, then d_v / (16 TPW) for B_seg, all
+// on one XCD.  Only segments that another segment of the same sequence
+// follows get a map; the first segment's A only when there is an initial
+// state.  A is stored in NM's fragment order (bf16) through an LDS transpose,
+// B_seg in fp32 in the state kernel's tile order (prefill.h).
+template <typename T, int DK, int DV, bool KDA, bool SINGLE, int TPW>
+__global__ __launch_bounds__(64 * (TPW + 1), 1) void seg_map_kernel(PrefillArgs a) {
+  static_assert(sizeof(T) == 2, "the staged walk is the bf16 path");
+  static_assert(TPW % 2 == 0, "A's fragment blocks pair adjacent column tiles");
+  using S = WalkStage<T, DK, KDA, false>;
+  constexpr int RT = DK / 16, KB = DK / 32;
+  constexpr int NA = DK / (16 * TPW), NB = DV / (16 * TPW);  // workgroups per map
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int b = blockIdx.x;
+  const int xcd = b % kXcds, slot = b / kXcds;
+  const int pair = (slot / (NA + NB)) * kXcds + xcd;  // (segment, value head)
+  const int part = slot % (NA + NB);                  // < NA: A, else B_seg
+  if (pair >= a.max_segs * a.Hv) return;  // uniform for the workgroup
+  const int sgi = pair / a.Hv, h = pair % a.Hv;
+  const int4 sg = seg_info_at<SINGLE>(a, sgi);  // {sequence, first chunk, chunks, index in sequence}
+  if (sg.x < 0) return;
+  if (sg.w == seq_seg_at<SINGLE>(a, sg.x).y - 1) return;  // the last segment's map is never applied
+  const bool apart = part < NA;
+  if (apart && sg.w == 0 && !a.s0) return;  // the first segment's A acts on the initial state only
+  const int nch = sg.z;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  auto blk = [&](int c) { return (size_t)(sg.y + min(c, nch - 1)) * a.Hv + h; };
+
+  if (wave == TPW) {
+    // ---- loader wave: chunk c into stage c % 3, two chunks ahead
+    if (nch > 0) {
+      const unsigned char *NMg = static_cast<const unsigned char *>(a.NM);
+      auto issue = [&](int c) {
+        const size_t bk = blk(c);
+        unsigned char *st = lds + (c % S::NSTAGE) * S::BYTES;
+        const unsigned char *nm = NMg + bk * S::NM_BYTES + lane * 16;
+#pragma unroll
+        for (int j = 0; j < S::NM_OPS; ++j) lds_load16(nm + j * 1024, st + j * 1024);
+        if constexpr (KDA) {
+#pragma unroll
+          for (int j = 0; j < S::DEC_OPS; ++j) lds_load4(a.dec + bk * DK + j * 64 + lane, st + S::NM_BYTES + j * 256);
+        }
+      };
+      issue(0);
+      issue(1);
+      wait_vmcnt<S::OPS>();  // chunk 0 has landed
+      walk_barrier();        // B_0
+      for (int k = 1; k <= nch; ++k) {
+        issue(k + 1);          // into the stage of chunk k - 2, whose reads ended before B_(k-1)
+        wait_vmcnt<S::OPS>();  // chunk k has landed (chunk k + 1 may be in flight)
+        walk_barrier();        // B_k
+      }
+      wait_vmcnt<0>();  // nothing in flight into LDS when the wave ends
+    }
+    walk_barrier();  // B_end: the tile waves' transpose may reuse the stages
+    return;
+  }
+
+  // ---- tile wave: column tile t of A (plain column indices 16t ..) or of
+  //      B_seg (the state's columns dv_of(t, ..))
+  const int t = (apart ? part : part - NA) * TPW + wave;
+  const int col = lane & 15, grp = lane >> 4;
+  f32x4 H[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) H[rt][e] = (apart && 16 * rt + 4 * grp + e == 16 * t + col) ? 1.f : 0.f;
+
+  if (nch > 0) {
+    const T *__restrict__ Bg = static_cast<const T *>(a.Bc);
+    struct Lane {
+      uint2 b[RT];  // B rows 16rt + 4grp .. +3 of tile t (B_seg walks only)
+      float dec;    // GDN decay of the chunk
+    };
+    auto fetch = [&](Lane &op, int c) {
+      const size_t bk = blk(c);
+      if (!apart) {
+        const T *bp = Bg + bk * ((size_t)DV * DK) + (size_t)(t * 64 + lane) * (DK / 4);
+#pragma unroll
+        for (int i = 0; i < DK / 32; ++i) {
+          const u32x4 v = *reinterpret_cast<const u32x4 *>(bp + 8 * i);
+          op.b[2 * i] = make_uint2(v[0], v[1]);
+          op.b[2 * i + 1] = make_uint2(v[2], v[3]);
+        }
+      } else {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) op.b[rt] = make_uint2(0u, 0u);
+      }
+      if constexpr (!KDA) op.dec = a.dec[bk * DK];
+    };
+    Lane ring[2];
+    fetch(ring[0], 0);
+    fetch(ring[1], 1);
+    Frag<T> f[2][RT];
+    auto read_nm = [&](const unsigned char *stl, int kb, int buf) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+        f[buf][rt] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(stl + (rt * KB + kb) * 1024));
+    };
+    const unsigned char *lds_lane = lds + lane * 16;
+    walk_barrier();  // B_0: chunk 0 is in stage 0
+    read_nm(lds_lane, 0, 0);
+    auto step = [&](auto slot_c, int c) {
+      constexpr int u = decltype(slot_c)::value;  // c & 1: operand ring slot
+      const unsigned char *stl = lds_lane + __builtin_amdgcn_readfirstlane((c % S::NSTAGE) * S::BYTES);
+      const unsigned char *stn = lds_lane + __builtin_amdgcn_readfirstlane(((c + 1) % S::NSTAGE) * S::BYTES);
+      Frag<T> hb[KB];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) hb[kb] = frag_from_acc<T>(H[2 * kb], H[2 * kb + 1]);
+      f32x4 dk[KDA ? RT : 1];
+      if constexpr (KDA) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+          dk[rt] = *reinterpret_cast<const f32x4 *>(stl - lane * 16 + S::NM_BYTES + (16 * rt + 4 * grp) * 4);
+      }
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const f32x4 d = KDA ? dk[KDA ? rt : 0] : f32x4{ring[u].dec, ring[u].dec, ring[u].dec, ring[u].dec};
+        H[rt] = d * H[rt] + raw4_to_f32(ring[u].b[rt]);
+      }
+      fetch(ring[u], c + 2);
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const int cur = kb & 1;
+        if (kb + 1 < KB) {
+          read_nm(stl, kb + 1, cur ^ 1);
+        } else {
+          walk_barrier();            // B_(c+1): chunk c + 1 landed; every read of stage c done
+          read_nm(stn, 0, cur ^ 1);  // KB is even: buffer 0
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) H[rt] = mma(H[rt], f[cur][rt], hb[kb]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    for (int c = 0; c < nch; c += 2) {
+      step(std::integral_constant<int, 0>{}, c);
+      if (c + 1 < nch) step(std::integral_constant<int, 1>{}, c + 1);  // uniform for the workgroup
+    }
+  }
+  walk_barrier();  // B_end: every stage read and every load landed
+
+  const size_t mblk = (size_t)sgi * a.Hv + h;
+  if (!apart) {
+    float *bm = a.Bseg + mblk * ((size_t)DK * DV);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+      *reinterpret_cast<f32x4 *>(bm + ((size_t)(t * RT + rt) * 64 + lane) * 4) = H[rt];
+    return;
+  }
+  // A: this workgroup's 16 TPW columns, rounded to bf16, row-major in LDS
+  // (rows padded by 8 elements), then stored as NM-ordered operand blocks
+  // (row tile rt, k-block kb): slot j of lane (col, grp) holds
+  // A[16rt + col][32kb + kmap(grp, j)]
+  constexpr int LD = 16 * TPW + 8;
+  T *sA = reinterpret_cast<T *>(lds);
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sA[(16 * rt + 4 * grp + e) * LD + 16 * wave + col] = Elt<T>::from_f32(H[rt][e]);
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  T *am = static_cast<T *>(a.Aseg) + mblk * ((size_t)DK * DK);
+  constexpr int KBW = TPW / 2;        // k-blocks of this workgroup
+  const int kb0 = part * KBW;         // first k-block of this workgroup
+  for (int q = wave; q < RT * KBW; q += TPW) {
+    const int rt = q / KBW, kbl = q % KBW;
+    const T *row = sA + (16 * rt + col) * LD + 32 * kbl + 4 * grp;
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[j] = Elt<T>::to_f32(row[j]);
+      x[4 + j] = Elt<T>::to_f32(row[16 + j]);
+    }
+    store_frag_at(am + ((size_t)(rt * KB + kb0 + kbl) * 64 + lane) * 8, make_frag<T>(x));
+  }
+}
+
+template <typename T, int DK, int DV, bool KDA, bool SINGLE, int TPW>
+static hipError_t launch_maps_t(const PrefillArgs &a, hipStream_t stream) {
+  using S = WalkStage<T, DK, KDA, false>;
+  constexpr int kMaxDevices = 64;
+  static std::atomic<bool> done[kMaxDevices];
+  const void *kern = reinterpret_cast<const void *>(&seg_map_kernel<T, DK, DV, KDA, SINGLE, TPW>);
+  constexpr int walk_lds = S::NSTAGE * S::BYTES;
+  constexpr int tr_lds = DK * (16 * TPW + 8) * (int)sizeof(T);
+  const int lds = walk_lds > tr_lds ? walk_lds : tr_lds;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices || !done[dev].load(std::memory_order_relaxed)) {
+    if ((e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds)) != hipSuccess) return e;
+    if (dev >= 0 && dev < kMaxDevices) done[dev].store(true, std::memory_order_relaxed);
+  }
+  const long items = (long)a.max_segs * a.Hv;
+  const long groups = (items + kXcds - 1) / kXcds;
+  const long blocks = groups * kXcds * (DK / (16 * TPW) + DV / (16 * TPW));
+  hipLaunchKernelGGL((seg_map_kernel<T, DK, DV, KDA, SINGLE, TPW>), dim3((unsigned)blocks), dim3(64 * (TPW + 1)), lds,
+                     stream, a);
+  return hipGetLastError();
+}
+
+template <int DK, int DV, bool KDA>
+hipError_t launch_maps_dims(const PrefillArgs &a, hipStream_t s) {
+  // as many tiles per workgroup as the narrower map has: fewer copies of each NM block
+  constexpr int TPW = (DK < DV ? DK : DV) / 16;
+  return a.single ? launch_maps_t<bf16_t, DK, DV, KDA, true, TPW>(a, s)
+                  : launch_maps_t<bf16_t, DK, DV, KDA, false, TPW>(a, s);
+}
+
+template <bool KDA>
+hipError_t launch_maps_kind(const PrefillArgs &a, hipStream_t s) {
+  if (a.Dk == 64 && a.Dv == 64) return launch_maps_dims<64, 64, KDA>(a, s);
+  if (a.Dk == 64 && a.Dv == 128) return launch_maps_dims<64, 128, KDA>(a, s);
+  if (a.Dk == 128 && a.Dv == 64) return launch_maps_dims<128, 64, KDA>(a, s);
+  return launch_maps_dims<128, 128, KDA>(a, s);
+}
+
 // The staged walk's LDS (three stages) exceeds the default 64 KiB limit: raise
 // it once per device and instance.
 template <typename T, int DK, int DV, bool KDA, bool SINGLE, int TPW>
@@ -324,6 +552,10 @@ hipError_t launch_walk_kind(const PrefillArgs &a, int cus, hipStream_t s) {
 }
 
 }  // namespace
+
+hipError_t launch_seg_maps(const PrefillArgs &a, bool kda, hipStream_t s) {
+  return kda ? launch_maps_kind<true>(a, s) : launch_maps_kind<false>(a, s);
+}
 
 hipError_t launch_state_walk(const PrefillArgs &a, bool kda, int cus, hipStream_t s) {
   return kda ? launch_walk_kind<true>(a, cus, s) : launch_walk_kind<false>(a, cus, s);

@@ -676,6 +676,7 @@ static hipError_t dispatch(const PrefillArgs &a, bool bf16, bool kda, hipStream_
 }
 
 hipError_t launch_seg_transfer(const PrefillArgs &a, bool bf16, bool kda, hipStream_t s) {
+  if (bf16) return launch_seg_maps(a, kda, s);
   return dispatch<true>(a, bf16, kda, s);
 }
 

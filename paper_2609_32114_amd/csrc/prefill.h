@@ -152,6 +152,8 @@ hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStrea
 // the bf16 whole-chain walk for batches with more walks than the device's
 // `cus` compute units (k2_walk.hip)
 hipError_t launch_state_walk(const PrefillArgs &a, bool kda, int cus, hipStream_t stream);
+// the bf16 segment maps on the staged walk (k2_walk.hip)
+hipError_t launch_seg_maps(const PrefillArgs &a, bool kda, hipStream_t stream);
 // segment-parallel path: segment maps, then ops #5 + #6 per segment
 hipError_t launch_seg_transfer(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
 hipError_t launch_seg_state(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);

@@ -50,6 +50,14 @@ def test_f32_segments(seg, kind, dims):
     check_against_oracle(inp, label=f"seg-f32 {kind} {dims}")
 
 
+@pytest.mark.parametrize("dims", [(64, 64), (64, 128), (128, 64)])
+@pytest.mark.parametrize("kind", ["gdn", "kda"])
+def test_bf16_segment_dims(seg, kind, dims):
+    seg(2)
+    inp = make_case(kind, (450, 130), 2, 4, dims[0], dims[1], "bf16", with_s0=True, seed=36)
+    check_against_oracle(inp, label=f"seg-bf16 {kind} {dims}")
+
+
 @pytest.mark.parametrize("L", [1, 2])
 @pytest.mark.parametrize("s0", [True, False])
 def test_varlen_segments(seg, L, s0):
