@@ -14,7 +14,9 @@
 //   seg_transfer  one workgroup per (segment, value head, part): runs the
 //                 segment's chunk chain on A (part 0, from I, no B term) or on
 //                 B_seg (part 1, from 0) and stores the segment map -- only for
-//                 segments that another segment of the same sequence follows;
+//                 segments that another segment of the same sequence follows
+//                 (fp32; the bf16 maps run on the staged walk, seg_map_kernel
+//                 in k2_walk.hip);
 //   seg_state     one workgroup per (segment, value head): applies the maps of
 //                 the earlier segments of its sequence to the initial state (a
 //                 short chain of d_k x d_k products), then walks its own
