@@ -63,16 +63,17 @@ constexpr long kCus = 256;  // compute units of an MI355X (gfx950)
 // head-resident workgroup moves a whole head's operands through one CU), on
 // about (n / L) Hv workgroups.  Measured on MI355X (1 sequence, d = 128, bf16,
 // operator totals): with 16 heads (128 walk workgroups) segments pay from
-// about 144 chunks (T = 9216: 217 us at L = 16 against 248 whole; T = 12288:
-// 286 against 349; T = 32768: 694 against 855), and the best L puts about
-// one segment workgroup on every CU (L = n Hv / 256, at least 12).  With 32
-// heads (256 walk workgroups) the whole walk still won at 256 chunks (604 us
-// against 682), so the threshold grows with the walks' share of the CUs.
-// KDA pays from fewer chunks: its per-channel gate adds 8 KiB per token
-// (d = 128) to the chunk-local kernel's input and pushes the walk's operands
-// out of the Infinity Cache sooner.  With 16 heads: T = 6144 185 us whole
-// against 186 at L = 12; T = 8192 249 against 230 at L = 8; T = 12288 395
-// against 331 at L = 12.  KDA segments from 112 chunks with L at least 8.
+// about 120 chunks (T = 6144: 135 us whole against 141 at L = 12; T = 8192:
+// 187 against 182 at L = 12; T = 9216: 235 against 200; T = 12288: 341
+// against 267), and the best L puts about one segment workgroup on every CU
+// (L = n Hv / 256, at least 12).  With 32 heads (256 walk workgroups) the
+// whole walk still won at 192 chunks (453 us against 485), so the threshold
+// grows with the walks' share of the CUs.  KDA pays from fewer chunks: its
+// per-channel gate adds 8 KiB per token (d = 128) to the chunk-local kernel's
+// input and pushes the walk's operands out of the Infinity Cache sooner.  With
+// 16 heads: T = 4096 128 us whole against 132 at L = 8; T = 6144 180 against
+// 176 at L = 8; T = 8192 251 against 217.  KDA segments from 88 chunks with L
+// at least 8.
 //
 // Whatever the choice (or override), L is capped so that the o rows of one
 // segment, 64 L Hv Dv elements, span less than 2 GiB: the walk kernels address
@@ -90,7 +91,7 @@ int seg_chunks(int N, int T, int Hv, int Dv, size_t esz, bool kda) {
     const long n_all = ((long)T + hagdn::kChunk - 1) / hagdn::kChunk;  // longest possible chain
     const long n_avg = ((long)T / (N > 0 ? N : 1) + hagdn::kChunk - 1) / hagdn::kChunk;
     const double walks = (double)(N > 0 ? N : 1) * Hv * std::max(1, Dv / 16);
-    const double threshold = (kda ? 112.0 : 144.0) * std::max(1.0, walks / (kCus / 2));
+    const double threshold = (kda ? 88.0 : 120.0) * std::max(1.0, walks / (kCus / 2));
     if ((double)n_avg < threshold) L = n_all > 0 ? std::min<long>(n_all, kMaxSegChunks) : 1;
     else L = std::max<long>(kda ? 8 : 12, (n_all * Hv + kCus - 1) / kCus);
   }

@@ -107,21 +107,24 @@ def test_segment_length_knob():
         assert P.segment_chunks(1, 256, 1, 64) == 4
         assert P.segment_chunks(1, 0, 1, 64) == 1
         assert P.segment_chunks(1, 4096, 16, 128) == 64
-        assert P.segment_chunks(1, 9151, 16, 128) == 143    # below 144 chunks: whole
+        assert P.segment_chunks(1, 7616, 16, 128) == 119    # below 120 chunks: whole
+        assert P.segment_chunks(1, 7680, 16, 128) == 12     # 120 chunks
         assert P.segment_chunks(1, 9216, 16, 128) == 12     # 144 chunks
         assert P.segment_chunks(1, 12288, 16, 128) == 12
         assert P.segment_chunks(1, 16384, 16, 128) == 16
         assert P.segment_chunks(1, 32768, 16, 128) == 32
         assert P.segment_chunks(1, 131072, 16, 128) == 128  # 2048 chunks
-        assert P.segment_chunks(1, 16384, 32, 128) == 256   # 256 walk workgroups: threshold 288
+        assert P.segment_chunks(1, 15296, 32, 128) == 239   # 256 walk workgroups: threshold 240
+        assert P.segment_chunks(1, 15360, 32, 128) == 30    # 240 chunks: 240 x 32 / 256
         assert P.segment_chunks(1, 18432, 32, 128) == 36    # 288 chunks: 288 x 32 / 256
         assert P.segment_chunks(8, 34816, 32, 128) == 544   # short average chains: whole
         # KDA segments from 112 chunks, L at least 8
-        assert P.segment_chunks(1, 7104, 16, 128, kind="kda") == 111
-        assert P.segment_chunks(1, 7168, 16, 128, kind="kda") == 8
+        assert P.segment_chunks(1, 5568, 16, 128, kind="kda") == 87
+        assert P.segment_chunks(1, 5632, 16, 128, kind="kda") == 8
         assert P.segment_chunks(1, 8192, 16, 128, kind="kda") == 8
         assert P.segment_chunks(1, 12288, 16, 128, kind="kda") == 12
-        assert P.segment_chunks(1, 8192, 16, 128, kind="gdn") == 128
+        assert P.segment_chunks(1, 8192, 16, 128, kind="gdn") == 12
+        assert P.segment_chunks(1, 6144, 16, 128, kind="gdn") == 96
         with pytest.raises(ValueError):
             P.segment_chunks(1, 8192, 16, 128, kind="mamba")
         P.set_segment_chunks(8)
