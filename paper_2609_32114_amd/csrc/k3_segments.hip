@@ -679,7 +679,7 @@ static hipError_t dispatch(const PrefillArgs &a, bool bf16, bool kda, hipStream_
 
 hipError_t launch_seg_transfer(const PrefillArgs &a, bool bf16, bool kda, hipStream_t s) {
   if (bf16) return launch_seg_maps(a, kda, s);
-  return dispatch<true>(a, bf16, kda, s);
+  return kda ? dispatch_dims<float, true, true>(a, s) : dispatch_dims<float, false, true>(a, s);
 }
 
 hipError_t launch_seg_state(const PrefillArgs &a, bool bf16, bool kda, hipStream_t s) {
