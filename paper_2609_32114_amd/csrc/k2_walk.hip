@@ -1,8 +1,13 @@
-// k2_walk.hip -- the bf16 path of the Reduce phase of chunkwise delta-rule
-// prefill (paper Sec. 2.1, operator #5 H) fused with the final Map (operator
-// #6 O), for chains walked whole: the staged walk.  The fp32 path and the
-// chunk affine map it applies are described in k2_state_prop.hip; chains long
-// enough for segment maps take k3_segments.hip instead.
+// k2_walk.hip -- staged walks (bf16): the Reduce phase of chunkwise
+// delta-rule prefill (paper Sec. 2.1, operator #5 H) with one wave per
+// 16-column tile and the chunk's shared operands staged in LDS by a loader
+// wave.  Two kernels:
+//   state_walk_kernel  operators #5 and #6 over whole chains, for batches with
+//                      more walks than CUs (k2_state_prop.hip walks the
+//                      others, and every fp32 chain);
+//   seg_map_kernel     the segment maps of the segment-parallel path (paper
+//                      Sec. 4, Chunk-Seg-Seg; the rest of it is in
+//                      k3_segments.hip).
 //
 // Per chunk c the chunk-local kernel has left
 //     S^T_{c+1} = D S^T_c + NM S^T_c + B,     O = scale (Q' S^T_c + O_loc)
@@ -10,9 +15,9 @@
 // "Computation Splitting"): the d_v columns of S^T evolve independently, so a
 // head splits into d_v/16 chains with no reduction between them.
 //
-// Workgroup -> (pair, tile group) mapping is XCD-aware: consecutive workgroup
-// ids are dealt round-robin to the 8 XCDs, so all tile groups of one
-// (sequence, head) pair share one XCD and its L2 for NM and Q'.
+// Workgroup -> work mapping is XCD-aware: consecutive workgroup ids are dealt
+// round-robin to the 8 XCDs, so all workgroups of one (sequence, head) pair
+// or (segment, head) pair share one XCD and its L2.
 #include <atomic>
 #include <type_traits>
 
