@@ -204,6 +204,7 @@ MANY_WALKS = [
     ("gdn", (100, 37), 4, 80, 64, 64),
     ("kda", (90, 40), 4, 96, 64, 64),
     ("kda", (150,), 2, 40, 64, 128),
+    ("kda", (200,), 4, 80, 128, 128),
 ]
 
 
