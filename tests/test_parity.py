@@ -205,7 +205,7 @@ MANY_WALKS = [
     ("kda", (90, 40), 4, 96, 64, 64),
     ("kda", (150,), 2, 40, 64, 128),
     ("kda", (200,), 4, 80, 128, 128),
-    # more than four times as many: eight tiles per workgroup, no loader wave
+    # more than four walks per CU
     ("gdn", (150,), 8, 160, 128, 128),
     ("gdn", (90, 60), 4, 80, 64, 128),
 ]
