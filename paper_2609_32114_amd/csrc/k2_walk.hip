@@ -60,10 +60,13 @@ __device__ __forceinline__ void walk_store4(__amdgpu_buffer_rsrc_t r, int off, f
 // workgroup and its stages.  Each tile wave fetches its own B and O_loc (and
 // the GDN decay) into registers two chunks ahead.
 //
-// One step of a tile wave: B_c (barrier: stage c landed, stage c-1 free) ->
-// S_c as bf16 B fragments -> o of chunk c-1 stored -> S <- D S + B ->
-// for each k-block: S += NM(:, kb) S_c(kb) and O^T += S_c(kb) Q'(:, kb)^T,
-// the LDS operand reads running one k-block ahead of the products.
+// One step c of a tile wave: S_c as bf16 B fragments -> S <- D S + B -> o of
+// chunk c-1 stored -> for each k-block kb: S += NM(:, kb) S_c(kb) and
+// O^T += S_c(kb) Q'(:, kb)^T, with the NM fragments of k-block kb+1 read from
+// LDS ahead of the products.  Before the last k-block comes the step's one
+// barrier, B_(c+1): chunk c+1 has landed and every read of stage c is done
+// (the loader then refills it), and chunk c+1's first fragments are read
+// behind it while the last products run.
 template <typename T, int DK, bool KDA, bool QP = true>
 struct WalkStage {
   static constexpr int NM_BYTES = DK * DK * (int)sizeof(T);
@@ -96,9 +99,6 @@ __device__ __forceinline__ void walk_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-}
-__device__ __forceinline__ bf16x8 lds_frag16(const unsigned char *region, int blockno, int lane) {
-  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(region + (blockno * 64 + lane) * 16));
 }
 
 template <typename T, int DK>
@@ -211,7 +211,8 @@ __global__ __launch_bounds__(64 * (TPW + 1), 1) void state_walk_kernel(PrefillAr
     // NM fragments of one k-block (row tiles), read one k-block ahead; the
     // next chunk's first k-block is read behind the barrier that publishes
     // its stage, before this chunk's last products.  Q' fragments (token
-    // tiles) are read at the start of their k-block, behind its NM products.
+    // tiles) are read at the start of their k-block and used after its NM
+    // products.
     Frag<T> f[2][RT];
     auto read_nm = [&](const unsigned char *stl, int kb, int buf) {
 #pragma unroll
