@@ -5,9 +5,10 @@
 //   state_walk_kernel  operators #5 and #6 over whole chains, for batches with
 //                      more walks than CUs (k2_state_prop.hip walks the
 //                      others, and every fp32 chain);
-//   seg_map_kernel     the segment maps of the segment-parallel path (paper
-//                      Sec. 4, Chunk-Seg-Seg; the rest of it is in
-//                      k3_segments.hip).
+//   seg_pair_kernel,   the segment maps of the segment-parallel path (paper
+//   seg_map_kernel     Sec. 4, Chunk-Seg-Seg; the rest of it is in
+//                      k3_segments.hip): both maps of a segment in one
+//                      workgroup when d_k = d_v, else one workgroup per map.
 //
 // Per chunk c the chunk-local kernel has left
 //     S^T_{c+1} = D S^T_c + NM S^T_c + B,     O = scale (Q' S^T_c + O_loc)
@@ -470,6 +471,197 @@ __global__ __launch_bounds__(64 * (TPW + 1), 1) void seg_map_kernel(PrefillArgs 
   }
 }
 
+// Both maps of a segment in one workgroup (d_k = d_v = D): wave w walks
+// column tile w of A and column tile w of B_seg side by side, so every NM
+// fragment it reads from LDS feeds two products and each NM block crosses
+// the CU once per step.  With D/16 waves of about 200 registers a loader wave
+// would not fit beside them, so the waves issue the stage loads themselves
+// (load j by wave j mod D/16), as the last memory operations of a step, and
+// wait for their share of the next chunk before its barrier.
+template <typename T, int D, bool KDA, bool SINGLE>
+__global__ __launch_bounds__(64 * (D / 16), 1) void seg_pair_kernel(PrefillArgs a) {
+  static_assert(sizeof(T) == 2, "the staged walk is the bf16 path");
+  using S = WalkStage<T, D, KDA, false>;
+  constexpr int NW = D / 16, RT = D / 16, KB = D / 32;
+  constexpr int SHARE = S::OPS / NW;  // fewest stage loads of one wave per chunk
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int pair = blockIdx.x;  // (segment, value head): nothing shared between workgroups
+  if (pair >= a.max_segs * a.Hv) return;  // uniform for the workgroup
+  const int sgi = pair / a.Hv, h = pair % a.Hv;
+  const int4 sg = seg_info_at<SINGLE>(a, sgi);  // {sequence, first chunk, chunks, index in sequence}
+  if (sg.x < 0) return;
+  if (sg.w == seq_seg_at<SINGLE>(a, sg.x).y - 1) return;  // the last segment's map is never applied
+  const bool do_a = sg.w > 0 || a.s0;  // the first segment's A acts on the initial state only
+  const int nch = sg.z;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int col = lane & 15, grp = lane >> 4;
+  auto blk = [&](int c) { return (size_t)(sg.y + min(c, nch - 1)) * a.Hv + h; };
+  const unsigned char *NMg = static_cast<const unsigned char *>(a.NM);
+  auto issue_share = [&](int c) {
+    const size_t bk = blk(c);
+    unsigned char *st = lds + (c % S::NSTAGE) * S::BYTES;
+    for (int j = w; j < S::OPS; j += NW) {  // uniform for the wave
+      if (j < S::NM_OPS) {
+        lds_load16(NMg + bk * S::NM_BYTES + lane * 16 + j * 1024, st + j * 1024);
+      } else {
+        const int q = j - S::NM_OPS;
+        lds_load4(a.dec + bk * D + q * 64 + lane, st + S::NM_BYTES + q * 256);
+      }
+    }
+  };
+
+  f32x4 HA[RT], HB[RT];  // tile w of A (columns 16w + col) and of B_seg (columns dv_of(w, col))
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      HA[rt][e] = (16 * rt + 4 * grp + e == 16 * w + col) ? 1.f : 0.f;
+      HB[rt][e] = 0.f;
+    }
+
+  if (nch > 0) {
+    const T *__restrict__ Bg = static_cast<const T *>(a.Bc);
+    struct Lane {
+      uint2 b[RT];  // B rows 16rt + 4grp .. +3 of tile w
+      float dec;    // GDN decay of the chunk
+    };
+    auto fetch = [&](Lane &op, int c) {
+      const size_t bk = blk(c);
+      const T *bp = Bg + bk * ((size_t)D * D) + (size_t)(w * 64 + lane) * (D / 4);
+#pragma unroll
+      for (int i = 0; i < D / 32; ++i) {
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(bp + 8 * i);
+        op.b[2 * i] = make_uint2(v[0], v[1]);
+        op.b[2 * i + 1] = make_uint2(v[2], v[3]);
+      }
+      if constexpr (!KDA) op.dec = a.dec[bk * D];
+    };
+    Lane ring[2];
+    fetch(ring[0], 0);
+    fetch(ring[1], 1);
+    __builtin_amdgcn_sched_barrier(0);
+    issue_share(0);
+    issue_share(1);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vmcnt<SHARE>();  // this wave's share of chunk 0 has landed
+    Frag<T> f[2][RT];
+    auto read_nm = [&](const unsigned char *stl, int kb, int buf) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+        f[buf][rt] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(stl + (rt * KB + kb) * 1024));
+    };
+    const unsigned char *lds_lane = lds + lane * 16;
+    walk_barrier();  // B_0: chunk 0 is in stage 0
+    read_nm(lds_lane, 0, 0);
+    auto step = [&](auto slot_c, int c) {
+      constexpr int u = decltype(slot_c)::value;  // c & 1: operand ring slot
+      const unsigned char *stl = lds_lane + __builtin_amdgcn_readfirstlane((c % S::NSTAGE) * S::BYTES);
+      const unsigned char *stn = lds_lane + __builtin_amdgcn_readfirstlane(((c + 1) % S::NSTAGE) * S::BYTES);
+      Frag<T> ha[KB], hb[KB];
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        ha[kb] = frag_from_acc<T>(HA[2 * kb], HA[2 * kb + 1]);
+        hb[kb] = frag_from_acc<T>(HB[2 * kb], HB[2 * kb + 1]);
+      }
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        f32x4 d;
+        if constexpr (KDA) {
+          d = *reinterpret_cast<const f32x4 *>(stl - lane * 16 + S::NM_BYTES + (16 * rt + 4 * grp) * 4);
+        } else {
+          d = f32x4{ring[u].dec, ring[u].dec, ring[u].dec, ring[u].dec};
+        }
+        HA[rt] = d * HA[rt];
+        HB[rt] = d * HB[rt] + raw4_to_f32(ring[u].b[rt]);
+      }
+      fetch(ring[u], c + 2);
+      // this wave's share of chunk c + 2, into the stage step c - 1 read: the
+      // last memory operations of the step, so that the wait below leaves
+      // only them in flight
+      __builtin_amdgcn_sched_barrier(0);
+      issue_share(c + 2);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const int cur = kb & 1;
+        if (kb + 1 < KB) {
+          read_nm(stl, kb + 1, cur ^ 1);
+        } else {
+          wait_vmcnt<SHARE>();       // this wave's share of chunk c + 1 has landed
+          walk_barrier();            // B_(c+1): chunk c + 1 landed; every read of stage c done
+          read_nm(stn, 0, cur ^ 1);  // KB is even: buffer 0
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+          HA[rt] = mma(HA[rt], f[cur][rt], ha[kb]);
+          HB[rt] = mma(HB[rt], f[cur][rt], hb[kb]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    for (int c = 0; c < nch; c += 2) {
+      step(std::integral_constant<int, 0>{}, c);
+      if (c + 1 < nch) step(std::integral_constant<int, 1>{}, c + 1);  // uniform for the workgroup
+    }
+    wait_vmcnt<0>();  // nothing in flight into LDS
+  }
+  walk_barrier();  // B_end: every stage read and every load landed
+
+  const size_t mblk = (size_t)sgi * a.Hv + h;
+  float *bm = a.Bseg + mblk * ((size_t)D * D);
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) *reinterpret_cast<f32x4 *>(bm + ((size_t)(w * RT + rt) * 64 + lane) * 4) = HB[rt];
+  if (!do_a) return;  // uniform for the workgroup
+  // A rounded to bf16, row-major in LDS (rows padded by 8 elements), then
+  // stored as NM-ordered operand blocks (row tile rt, k-block kb): slot j of
+  // lane (col, grp) holds A[16rt + col][32kb + kmap(grp, j)]
+  constexpr int LD = D + 8;
+  T *sA = reinterpret_cast<T *>(lds);
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sA[(16 * rt + 4 * grp + e) * LD + 16 * w + col] = Elt<T>::from_f32(HA[rt][e]);
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+  T *am = static_cast<T *>(a.Aseg) + mblk * ((size_t)D * D);
+  for (int q = w; q < RT * KB; q += NW) {
+    const int rt = q / KB, kb = q % KB;
+    const T *row = sA + (16 * rt + col) * LD + 32 * kb + 4 * grp;
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[j] = Elt<T>::to_f32(row[j]);
+      x[4 + j] = Elt<T>::to_f32(row[16 + j]);
+    }
+    store_frag_at(am + ((size_t)(rt * KB + kb) * 64 + lane) * 8, make_frag<T>(x));
+  }
+}
+
+template <typename T, int D, bool KDA, bool SINGLE>
+static hipError_t launch_pair_t(const PrefillArgs &a, hipStream_t stream) {
+  using S = WalkStage<T, D, KDA, false>;
+  constexpr int kMaxDevices = 64;
+  static std::atomic<bool> done[kMaxDevices];
+  const void *kern = reinterpret_cast<const void *>(&seg_pair_kernel<T, D, KDA, SINGLE>);
+  constexpr int walk_lds = S::NSTAGE * S::BYTES;
+  constexpr int tr_lds = D * (D + 8) * (int)sizeof(T);
+  const int lds = walk_lds > tr_lds ? walk_lds : tr_lds;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices || !done[dev].load(std::memory_order_relaxed)) {
+    if ((e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds)) != hipSuccess) return e;
+    if (dev >= 0 && dev < kMaxDevices) done[dev].store(true, std::memory_order_relaxed);
+  }
+  const long blocks = (long)a.max_segs * a.Hv;
+  hipLaunchKernelGGL((seg_pair_kernel<T, D, KDA, SINGLE>), dim3((unsigned)blocks), dim3(64 * (D / 16)), lds, stream,
+                     a);
+  return hipGetLastError();
+}
+
 template <typename T, int DK, int DV, bool KDA, bool SINGLE, int TPW>
 static hipError_t launch_maps_t(const PrefillArgs &a, hipStream_t stream) {
   using S = WalkStage<T, DK, KDA, false>;
@@ -496,6 +688,8 @@ static hipError_t launch_maps_t(const PrefillArgs &a, hipStream_t stream) {
 
 template <int DK, int DV, bool KDA>
 hipError_t launch_maps_dims(const PrefillArgs &a, hipStream_t s) {
+  if constexpr (DK == DV)
+    return a.single ? launch_pair_t<bf16_t, DK, KDA, true>(a, s) : launch_pair_t<bf16_t, DK, KDA, false>(a, s);
   // as many tiles per workgroup as the narrower map has: fewer copies of each NM block
   constexpr int TPW = (DK < DV ? DK : DV) / 16;
   return a.single ? launch_maps_t<bf16_t, DK, DV, KDA, true, TPW>(a, s)
