@@ -67,8 +67,9 @@ constexpr long kCus = 256;  // compute units of an MI355X (gfx950)
 // 187 against 182 at L = 12; T = 9216: 235 against 200; T = 12288: 341
 // against 267), and the best L puts about one segment workgroup on every CU
 // (L = n Hv / 256, at least 12).  With 32 heads (256 walk workgroups) the
-// whole walk still won at 192 chunks (453 us against 485), so the threshold
-// grows with the walks' share of the CUs.  KDA pays from fewer chunks: its
+// whole walk still won at 256 chunks (T = 16384: 596 us against 619 at
+// L = 32; 192 chunks: 484 against 480), so the threshold grows with the
+// walks' share of the CUs, r = walks / 128: 120 r + 48 (r - 1) chunks.  KDA pays from fewer chunks: its
 // per-channel gate adds 8 KiB per token (d = 128) to the chunk-local kernel's
 // input and pushes the walk's operands out of the Infinity Cache sooner.  With
 // 16 heads: T = 4096 128 us whole against 132 at L = 8; T = 6144 180 against
@@ -91,7 +92,8 @@ int seg_chunks(int N, int T, int Hv, int Dv, size_t esz, bool kda) {
     const long n_all = ((long)T + hagdn::kChunk - 1) / hagdn::kChunk;  // longest possible chain
     const long n_avg = ((long)T / (N > 0 ? N : 1) + hagdn::kChunk - 1) / hagdn::kChunk;
     const double walks = (double)(N > 0 ? N : 1) * Hv * std::max(1, Dv / 16);
-    const double threshold = (kda ? 88.0 : 120.0) * std::max(1.0, walks / (kCus / 2));
+    const double r = std::max(1.0, walks / (kCus / 2));
+    const double threshold = (kda ? 88.0 : 120.0) * r + 48.0 * (r - 1.0);
     if ((double)n_avg < threshold) L = n_all > 0 ? std::min<long>(n_all, kMaxSegChunks) : 1;
     else L = std::max<long>(kda ? 8 : 12, (n_all * Hv + kCus - 1) / kCus);
   }

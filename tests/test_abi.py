@@ -114,8 +114,8 @@ def test_segment_length_knob():
         assert P.segment_chunks(1, 16384, 16, 128) == 16
         assert P.segment_chunks(1, 32768, 16, 128) == 32
         assert P.segment_chunks(1, 131072, 16, 128) == 128  # 2048 chunks
-        assert P.segment_chunks(1, 15296, 32, 128) == 239   # 256 walk workgroups: threshold 240
-        assert P.segment_chunks(1, 15360, 32, 128) == 30    # 240 chunks: 240 x 32 / 256
+        assert P.segment_chunks(1, 16384, 32, 128) == 256   # 256 walk workgroups: threshold 288
+        assert P.segment_chunks(1, 18368, 32, 128) == 287
         assert P.segment_chunks(1, 18432, 32, 128) == 36    # 288 chunks: 288 x 32 / 256
         assert P.segment_chunks(8, 34816, 32, 128) == 544   # short average chains: whole
         # KDA segments from 112 chunks, L at least 8
