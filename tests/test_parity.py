@@ -147,8 +147,14 @@ def test_bad_seqlens_single_sequence(kind):
     check_against_oracle(inp, label="after bad seqlens")
 
 
-def test_bitwise_deterministic():
-    inp = make_case("gdn", (1000, 333), 2, 4, 128, 128, "bf16", with_s0=True, seed=8)
+@pytest.mark.parametrize("case", [
+    ("gdn", (1000, 333), 2, 4),          # four-wave walk
+    ("gdn", (300, 200, 150), 8, 16),     # staged walk, two tiles per workgroup
+    ("kda", (130, 70, 200, 65), 8, 40),  # staged walk, four tiles per workgroup
+], ids=lambda c: f"{c[0]}-N{len(c[1])}-Hv{c[3]}")
+def test_bitwise_deterministic(case):
+    kind, lengths, Hqk, Hv = case
+    inp = make_case(kind, lengths, Hqk, Hv, 128, 128, "bf16", with_s0=True, seed=8)
     d = to_device(inp)
     a = run_gpu(inp, dev=d)
     b = run_gpu(inp, dev=d)

@@ -67,9 +67,10 @@ def test_varlen_segments(seg, L, s0):
     check_against_oracle(inp, label=f"seg-varlen L={L}")
 
 
-def test_segments_deterministic(seg):
+@pytest.mark.parametrize("kind", ["gdn", "kda"])
+def test_segments_deterministic(seg, kind):
     seg(3)
-    inp = make_case("gdn", (900, 333), 2, 4, 128, 128, "bf16", with_s0=True, seed=35)
+    inp = make_case(kind, (900, 333), 2, 4, 128, 128, "bf16", with_s0=True, seed=35)
     d = to_device(inp)
     a = run_gpu(inp, dev=d)
     b = run_gpu(inp, dev=d)
