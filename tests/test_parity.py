@@ -190,8 +190,16 @@ def test_workload2_shape_stress(variant):
     check_against_oracle(inp, heads=[4], label=f"workload2-{variant}")
 
 
-# More walk workgroups than CUs (N x Hv x Dv/16 > 256): bf16 walks pair
-# adjacent tiles in one workgroup, and walks share CUs.
+@pytest.mark.parametrize("variant", ["lm", "dn", "ks"])
+def test_workload4_shape_stress(variant):
+    """Workload 4's shape (2048 walks: the staged walk, four tiles per
+    workgroup) with gates that carry the state across every chunk."""
+    inp = make_workload(4, variant=variant)
+    check_against_oracle(inp, heads=[5, 26], label=f"workload4-{variant}")
+
+
+# More walk workgroups than CUs (N x Hv x Dv/16 > 256): bf16 chains take the
+# staged walk, two or four column tiles per workgroup.
 # Long-memory gates so that the state carries across every chunk; the oracle
 # checks every head.
 MANY_WALKS = [
