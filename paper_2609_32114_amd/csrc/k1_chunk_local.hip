@@ -227,10 +227,11 @@ struct LocalIn {
   // four waves (channel quarters): their partial sums of squares meet in
   // `scratch` (256 floats, one barrier) and the keys are rescaled in
   // registers before they are staged.  A query row lives in the four lane
-  // groups of one column (two lane exchanges); its factor is returned and
-  // applied to the products the queries enter (P and Q * e^gamma), which is
-  // the same as scaling the query rows.
-  __device__ __forceinline__ float l2norm_qk(float *scratch) {
+  // groups of one column (two lane exchanges); its factor is applied to the
+  // products the queries enter (P and Q * e^gamma), which is the same as
+  // scaling the query rows, and is formed only when op #2 needs it, so the
+  // query loads are waited for no earlier.
+  __device__ __forceinline__ void l2norm_k(float *scratch) {
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     using V16 = Vec16<T>;
     float ss = 0.f;
@@ -244,16 +245,6 @@ struct LocalIn {
       }
     }
     scratch[wave * 64 + lane] = ss;
-    float qs = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < DK / 32; ++kb)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float x = frag_elem(qf[kb], j);
-        qs += x * x;
-      }
-    qs += __shfl_xor(qs, 16);
-    qs += __shfl_xor(qs, 32);
     __syncthreads();
     const float ik = inv_l2(scratch[lane] + scratch[64 + lane] + scratch[128 + lane] + scratch[192 + lane]);
 #pragma unroll
@@ -264,6 +255,18 @@ struct LocalIn {
       for (int j = 0; j < V; ++j) x[j] = V16::get(u, j) * ik;
       kv[i] = __builtin_bit_cast(u32x4, V16::pack(x));
     }
+  }
+  __device__ __forceinline__ float l2norm_q() const {
+    float qs = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < DK / 32; ++kb)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float x = frag_elem(qf[kb], j);
+        qs += x * x;
+      }
+    qs += __shfl_xor(qs, 16);
+    qs += __shfl_xor(qs, 32);
     return inv_l2(qs);
   }
 };
@@ -311,9 +314,9 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
   const float bval = in.bval;
 
   // raw projections: normalise q and k (region Y is free until op #2)
-  float qscale = 1.f;  // L2 factor of this lane's query row rq (raw queries)
+  float qscale = 1.f;  // L2 factor of this lane's query row rq (raw queries), set before op #2
   if constexpr (PRE) {
-    if (a.pre & kPreQkNorm) qscale = in.l2norm_qk(sA);
+    if (a.pre & kPreQkNorm) in.l2norm_k(sA);
   }
 
   // ---- stage K (token rows; its channel rows follow op #2 in the same
@@ -364,6 +367,9 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
   //      A goes to LDS row-major (A[r][s], 4 consecutive s per lane); the P^T
   //      accumulators stay in registers: two of them form the P^T fragment of
   //      a 32-token k-block (accumulator slot map), the B operand of Q' and O_loc.
+  if constexpr (PRE) {
+    if (a.pre & kPreQkNorm) qscale = in.l2norm_q();
+  }
   f32x4 accP[4];
   {
     const int i = wave, r = rq;
