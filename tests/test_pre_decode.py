@@ -77,6 +77,35 @@ def test_prefill_preprocessing_matches_oracle(case):
     _check("s_final", sf, rs, TOL[dtype])
 
 
+# the flagged chunk-local instance feeding the other chain kernels: the bf16
+# segment maps (forced short segments) and the staged walk (more walks than
+# compute units: 3 sequences x 12 heads x 8 column tiles = 320 walks)
+PRE_CHAIN_CASES = [
+    # kind, lengths, Hqk, Hv, segment chunks (0: automatic)
+    ("kda", (700,), 2, 4, 3),
+    ("gdn", (400, 130), 2, 4, 2),
+    ("gdn", (130, 257, 64), 4, 12, 0),
+]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case", PRE_CHAIN_CASES, ids=[f"{c[0]}-L{c[4]}-{i}" for i, c in enumerate(PRE_CHAIN_CASES)])
+def test_prefill_preprocessing_through_segments_and_staged_walk(case):
+    import paper_2609_32114_amd as P
+    kind, lengths, Hqk, Hv, L = case
+    raw = inputs.make_case(kind=kind, lengths=lengths, Hqk=Hqk, Hv=Hv, Dk=128, Dv=128, dtype="bf16",
+                           with_s0=True, seed=78, raw=True)
+    say(f"[gpu] prefill pre={ALL} kind={kind} lengths={lengths} Hqk={Hqk} Hv={Hv} segment_chunks={L}")
+    P.set_segment_chunks(L)
+    try:
+        o, sf = _run_prefill_pre(raw, ALL)
+    finally:
+        P.set_segment_chunks(0)
+    ro, rs = oracle.run_inputs(raw, nthreads=oracle_threads(), pre=ALL)
+    _check("o", o, ro, TOL["bf16"])
+    _check("s_final", sf, rs, TOL["bf16"])
+
+
 def test_prefill_preprocessing_workload1_sampled_heads():
     """Workload 1 (T=4096, H=16, d=128, bf16) from raw projections, every flag,
     in the launch configuration the benchmark times; heads 0 and 11 checked."""
