@@ -21,6 +21,23 @@ preprocessing flag (q/k L2 normalisation, softplus gate, sigmoid beta).
 (H = 16, d = 128, bf16, fp32 state pool updated in place); its metric is
 decode tokens/s.
 
+Roofline fields (one JSON line):
+  roofline        the dominant kernel (longest HIP-event mean): the whole call's
+                  algorithmic bytes (q, k, v, gates, beta, s0 in; o, s_final out:
+                  16,512 B per token at the timed workload plus the states) over
+                  that kernel's mean duration, against 8 TB/s; traffic = the
+                  kernel's rocprofv3 FETCH_SIZE + WRITE_SIZE bytes per launch
+                  (copy-calibrated, profiles/traffic.json) while its sources are
+                  unchanged, else null
+  path_roofline   the same algorithmic bytes and FLOPs over the whole step
+  kernels         per kernel: mean ms, compulsory and counter bytes, HBM
+                  fractions of both, counter MFMA FLOPs and their fraction of the
+                  bf16 peak (counters from profiles/traffic.json, null when stale)
+  step_ms         mean of the timed steps, and median / p10 / p90 from a pass
+                  with one event between steps
+  peaks           published peaks and the ones measured in this run with the
+                  library's own streaming copy and bf16 MFMA loop
+
 Prints ONE JSON line.
 """
 
@@ -57,8 +74,9 @@ def kernel_source_hash(name: str) -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str, workload: str):
-    """HBM bytes per launch from committed rocprofv3 PMC counts, if still current."""
+def counter_record(kernel: str, workload: str):
+    """The committed rocprofv3 counter record of a kernel at a workload, if its
+    sources are unchanged since the counters were taken."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f).get(f"{kernel}@{workload}")
@@ -66,10 +84,49 @@ def measured_traffic(kernel: str, workload: str):
         return None
     if not rec or rec.get("source_hash") != kernel_source_hash(kernel):
         return None
-    return rec.get("bytes_per_launch")
+    return rec
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from committed rocprofv3 PMC counts, if still current."""
+    rec = counter_record(kernel, workload)
+    return None if rec is None else rec.get("bytes_per_launch")
+
+
+def kernel_table(kernel_ms, workload, compulsory):
+    """Per kernel: mean ms, compulsory / counter bytes and their HBM fractions,
+    counter MFMA FLOPs and their fraction of the bf16 peak."""
+    out = {}
+    for k, ms in kernel_ms.items():
+        if ms <= 0:
+            continue
+        rec = counter_record(k, workload) or {}
+        cb, fl = rec.get("bytes_per_launch"), rec.get("mfma_flops")
+        comp = compulsory(k)
+        out[k] = {"ms": ms, "compulsory_bytes": comp,
+                  "hbm_frac_compulsory": comp / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                  "counter_bytes": cb,
+                  "hbm_frac_counter": None if cb is None else cb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                  "mfma_flops_counter": fl,
+                  "mfma_frac_counter": None if fl is None else fl / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+                  "mfma_busy_counter": rec.get("mfma_busy")}
+    return out
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(inp, budget_s=10.0, max_reps=400, pre=0):
+    """The fp64 oracle on the host's cores (all the process may use, at most 16),
+    repeated over the full workload for about budget_s; then once on one thread."""
     import oracle
     threads = max(1, min(16, len(os.sched_getaffinity(0))))
     oracle.build(force=False)
@@ -81,9 +138,40 @@ def cpu_baseline(inp, budget_s=10.0, max_reps=400, pre=0):
         if el >= budget_s or reps >= max_reps:
             break
     tokens = reps * inp.T
+    t1 = time.perf_counter()
+    oracle.run_inputs(inp, nthreads=1, pre=pre)
+    el1 = time.perf_counter() - t1
     return {"value": tokens / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"full workload ({inp.T} tokens x {inp.v.shape[1]} heads) repeated "
-                      f"{reps}x, {el:.1f} s, fp64 token recurrence"}
+                      f"{reps}x, {el:.1f} s, fp64 token recurrence",
+            "cpu_model": cpu_model(), "value_1thread": inp.T / el1, "seconds_1thread": el1}
+
+
+def measured_peaks(P, torch, copy_mib=1024, mfma_iters=20000):
+    """HBM bandwidth of the library's streaming copy (read + write bytes / time)
+    and the bf16 rate of its MFMA loop, each the best of six event-timed runs."""
+    src = torch.empty(copy_mib << 18, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    dst = torch.empty_like(src)
+    n = src.numel() * 4
+    sink = torch.empty(16 * 1024, dtype=torch.float32, device="cuda:0")
+    best_copy = best_mfma = 0.0
+    for _ in range(6):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        P.measure_copy(src, dst)
+        b.record()
+        torch.cuda.synchronize()
+        best_copy = max(best_copy, 2 * n / (a.elapsed_time(b) * 1e-3) / 1e9)
+        a.record()
+        flops = P.measure_mfma(mfma_iters, sink)
+        b.record()
+        torch.cuda.synchronize()
+        best_mfma = max(best_mfma, flops / (a.elapsed_time(b) * 1e-3) / 1e12)
+    del src, dst
+    return {"hbm_gbs": HBM_PEAK_GBS, "bf16_tflops": BF16_PEAK_TFLOPS,
+            "measured_copy_gbs": best_copy, "measured_bf16_tflops": best_mfma,
+            "copy_bytes": 2 * n, "note": "published peaks are the roofline denominators; the measured "
+                                         "ones are this device's own copy and MFMA-loop rates"}
 
 
 def main():
@@ -102,7 +190,18 @@ def main():
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (10 times): the known-size "
                          "reference that scales rocprofv3 FETCH_SIZE / WRITE_SIZE counts")
+    ap.add_argument("--calibrate-mfma", type=int, default=0, metavar="ITERS",
+                    help="only run the library's bf16 MFMA loop (ITERS rounds, 3 times): the "
+                         "known-FLOP reference for rocprofv3 MFMA counters")
     args = ap.parse_args()
+    if args.calibrate_mfma:
+        import torch
+        import paper_2609_32114_amd as P
+        sink = torch.empty(16 * 1024, dtype=torch.float32, device="cuda:0")
+        flops = [P.measure_mfma(args.calibrate_mfma, sink) for _ in range(3)]
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_mfma_flops_per_launch": flops[0], "launches": 3}), flush=True)
+        return
     if args.calibrate_copy:
         import torch
         n = args.calibrate_copy * (1 << 20) // 4
@@ -176,6 +275,16 @@ def main():
     end.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(end) / args.steps
+    # the same K steps with one event between consecutive steps: the per-step
+    # distribution (each event adds a little GPU time; the mean above has none)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    evs[0].record()
+    for i in range(args.steps):
+        step(args.warmup + i)
+        evs[i + 1].record()
+    torch.cuda.synchronize()
+    per_step = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+    pct = lambda p: per_step[min(len(per_step) - 1, int(round(p * (len(per_step) - 1))))]
     # the same K steps again with the library's HIP events around every kernel
     # (on the launch stream): per-kernel durations for the roofline
     P.profile_begin(args.steps)
@@ -186,14 +295,18 @@ def main():
     value = T / (ms * 1e-3)
     dom = max(kernel_ms, key=kernel_ms.get)
     L = P.segment_chunks(N, T, Hv, Dv, torch.bfloat16 if esz == 2 else torch.float32, kind=inp.kind)
-    dom_bytes = cost.kernel_bytes(dom, T, N, Hqk, Hv, Dk, Dv, esz, kda, inp.s0 is not None,
-                                  seg_chunks=L)
-    dom_ms = kernel_ms[dom]
-    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     wname = wl.name + (f"_pre{pre}" if pre else "")
-    traffic = measured_traffic(dom, wname)
     path_bytes = cost.algorithmic_bytes(T, N, Hqk, Hv, Dk, Dv, esz, kda, inp.s0 is not None)
     path_flops = cost.flops(T, Hv, 64, Dk, Dv)
+    dom_ms = kernel_ms[dom]
+    # the contract's roofline: the method's algorithmic bytes per launch over
+    # the dominant kernel's mean duration
+    achieved = path_bytes / (dom_ms * 1e-3) / 1e9
+    traffic = measured_traffic(dom, wname)
+    compulsory = lambda k: cost.kernel_bytes(k, T, N, Hqk, Hv, Dk, Dv, esz, kda, inp.s0 is not None,
+                                             seg_chunks=L)
+    kernels = kernel_table(kernel_ms, wname, compulsory)
+    peaks = measured_peaks(P, torch)
     out = {
         "metric": METRIC,
         "value": value,
@@ -213,14 +326,18 @@ def main():
                    "preprocess": pre},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "bytes_per_launch": dom_bytes, "kernel_ms": dom_ms},
+                     "algorithmic_bytes": path_bytes, "kernel_ms": dom_ms},
         "path_roofline": {"bound": "hbm", "algorithmic_bytes": path_bytes,
                           "achieved": path_bytes / (ms * 1e-3) / 1e9, "peak": HBM_PEAK_GBS,
                           "unit": "GB/s", "frac": path_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                           "flops": path_flops,
                           "mfma_frac": path_flops / (ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
+        "step_ms": {"mean": ms, "median": pct(0.5), "p10": pct(0.1), "p90": pct(0.9),
+                    "samples": args.steps},
+        "kernels": kernels,
         "kernels_ms": kernel_ms,
         "kernel_calls_timed": ncalls,
+        "peaks": peaks,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(inp, pre=pre)

@@ -29,12 +29,19 @@
  *   v, o        [T, Hv,  Dv]   dtype
  *   g (GDN)     [T, Hv]        fp32 log-gate, a_t = exp(g) (g <= 0 expected)
  *   g (KDA)     [T, Hv, Dk]    fp32 per-key-channel log-gate
+ *               Every finite g <= 0 is supported, i.e. every gate a in (0, 1]:
+ *               KDA's factored decay switches, per 16-token block, to an exact
+ *               form when some channel decays by more than e^40 over half a
+ *               block (paper Sec. 2.1, the KDA variant).  g = -inf (a = 0) or
+ *               NaN propagates NaN into the affected chunk's outputs.
  *   beta        [T, Hv]        fp32 write strength
  *   s0, s_final [N, Hv, Dk, Dv] fp32, the state stored as S^T (row = key
  *               channel, d_v contiguous).  s0 == NULL means a zero initial
  *               state; s_final == NULL skips writing the final state.
- *               s_final may alias s0 exactly (in-place update); no other
- *               aliasing between arguments is allowed.
+ *               s_final may alias s0 exactly (in-place update, on every
+ *               path: the segmented path reads s0 only in a launch before
+ *               the one that writes s_final); no other aliasing between
+ *               arguments is allowed.
  *   cu_seqlens  [N+1] int32, DEVICE memory: cu[0] = 0, cu[N] = T,
  *               nondecreasing.  Zero-length sequences are allowed.  Chunks
  *               restart at every sequence start; no chunk spans two sequences.
@@ -88,8 +95,11 @@ typedef enum { HAGDN_DEV_OK = 0, HAGDN_DEV_BAD_SEQLENS = 1 } hagdn_device_code;
  * a sequence can span more than one segment of the state chain (Sec. 4's
  * Chunk-Seg-Seg mapping; see hagdn_segment_chunks) it also holds one segment
  * map, Dk*Dk elements plus Dk*Dv floats, per (segment, value head) for
- * segments bounded by (T/64 + N) / L + N.  The size depends on the segment
- * length L in force (hagdn_set_segment_chunks): query it after setting. */
+ * segments bounded by (T/64 + N) / L + N, and a copy of s0 (Dk*Dv floats
+ * per sequence and value head).  The size depends on the segment length L in
+ * force (hagdn_set_segment_chunks) and on the current device's compute units
+ * (see hagdn_segment_chunks): query it after setting, with the device the
+ * call will run on current. */
 size_t gdn_prefill_workspace_size(int N, int T_total, int Hqk, int Hv, int Dk,
                                   int Dv, int dtype);
 
@@ -216,13 +226,70 @@ int hagdn_version(void);
  * HAGDN_EINVAL (chunks < 0 or > 2^20). */
 int hagdn_set_segment_chunks(int chunks);
 
-/* L that a call with these sizes and dtype would use now (kda: 0 for
- * gdn_prefill, 1 for kda_prefill); -1 on invalid sizes or dtype.  Automatic or
- * forced, L is capped at the largest value with 64 L Hv Dv elements of dtype
- * below 2 GiB, so the output rows of one segment stay addressable with 32-bit
- * byte offsets; the cap depends on Hv, Dv and dtype, never on T_total.  A
- * call whose sequences can be longer than L chunks takes the segmented path. */
+/* L that a call with these sizes and dtype would use now on the current
+ * device (kda: 0 for gdn_prefill, 1 for kda_prefill); -1 on invalid sizes or
+ * dtype.  The automatic choice depends on the device's compute-unit count
+ * (queried once per device; the prefill calls use the same query).  On a host
+ * where no HIP device can be queried, this and the workspace-size queries
+ * answer for a 256-CU MI355X.  Automatic or forced, L is capped at the
+ * largest value with 64 L Hv Dv elements of dtype below 2 GiB, so the output
+ * rows of one segment stay addressable with 32-bit byte offsets; the cap
+ * depends on Hv, Dv and dtype, never on T_total.  A call whose sequences can
+ * be longer than L chunks takes the segmented path. */
 int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv, int dtype, int kda);
+
+/* The same rule for a device of `cus` compute units (no device query): host
+ * logic only.  -1 on invalid arguments (cus < 1 included). */
+int hagdn_segment_chunks_for(int N, int T_total, int Hv, int Dv, int dtype, int kda, int cus);
+
+/* Measurement aids (no prefill or decode call uses them): the ceilings that
+ * roofline fractions can be quoted against, measured on the current device.
+ *   hagdn_measure_copy  enqueues one streaming copy of `bytes` (a multiple of
+ *       16; src, dst 16-byte aligned device buffers that do not overlap) on 8
+ *       workgroups per CU with nontemporal 16-byte accesses: time it with
+ *       events on `stream` for the HBM bandwidth a plain kernel reaches.
+ *   hagdn_measure_mfma  enqueues 4 x CUs workgroups of four waves, each wave
+ *       running `iterations` rounds (1 .. 2^24) of 8 independent
+ *       v_mfma_f32_16x16x32_bf16 chains; *flops receives the launch's floating
+ *       point operations (2 per multiply-add).  sink (device, >= 16 x CUs
+ *       floats) receives one value per wave.
+ * Both return a hagdn_status. */
+int hagdn_measure_copy(const void *src, void *dst, size_t bytes, void *stream);
+int hagdn_measure_mfma(int iterations, float *sink, size_t sink_floats, double *flops, void *stream);
+
+/* Debugging: where a prefill call with these sizes (kda: 0 gdn_prefill, 1
+ * kda_prefill) keeps its chunk-local factors inside the workspace, so that a
+ * test can read them after the call (they stay there until the workspace is
+ * reused).  *offset receives the region's byte offset from the workspace
+ * start and *bytes its size (padding included).  Per (chunk c, value head h)
+ * block blk = c * Hv + h, with chunk c of a single sequence covering tokens
+ * [64c, 64c + 64) (a batch: the chunks of sequence 0, then of sequence 1, ...),
+ * Kt = (K * e^(gamma_last - gamma))^T, W and U~ operators #4 and P the
+ * masked Q K^T of operator #2 (paper Sec. 2.1):
+ *   HAGDN_WS_NM     -Kt W        Dk x Dk elements of dtype per block
+ *   HAGDN_WS_B      Kt U~        Dk x Dv elements of dtype
+ *   HAGDN_WS_QP     Q e^gamma - P W   64 x Dk elements of dtype
+ *   HAGDN_WS_OLOC   P U~         64 x Dv elements of dtype
+ *   HAGDN_WS_DECAY  e^gamma_last Dk floats (GDN: the first only)
+ *   HAGDN_WS_SEG_A, HAGDN_WS_SEG_B  the segment maps (segmented calls only)
+ * in the MFMA fragment orders that the walk kernels read: NM and Q' as 16 x 32
+ * operand blocks of 64 lanes x 8 elements (lane = column + 16 x lane group,
+ * element j of lane group g holding k index 4g + j (j < 4) or 12 + 4g + j),
+ * B and O_loc lane-major per 16-column state tile with the tile's columns
+ * interleaved in pairs of tiles (csrc/prefill.h gives the exact maps).
+ * Returns HAGDN_OK or HAGDN_EINVAL.  Depends on the device like the
+ * workspace size. */
+typedef enum {
+  HAGDN_WS_NM = 0,
+  HAGDN_WS_B = 1,
+  HAGDN_WS_QP = 2,
+  HAGDN_WS_OLOC = 3,
+  HAGDN_WS_DECAY = 4,
+  HAGDN_WS_SEG_A = 5,
+  HAGDN_WS_SEG_B = 6
+} hagdn_ws_region;
+int hagdn_workspace_region(int kda, int N, int T_total, int Hqk, int Hv, int Dk, int Dv, int dtype,
+                           int region, size_t *offset, size_t *bytes);
 
 #ifdef __cplusplus
 }

@@ -28,7 +28,8 @@ import os
 
 __all__ = ["gdn_prefill", "kda_prefill", "gdn_decode", "kda_decode", "workspace_size",
            "device_status", "library_path", "load_library", "profile_begin", "profile_end", "kernel_names", "set_segment_chunks",
-           "segment_chunks", "HagdnError"]
+           "segment_chunks", "segment_chunks_for", "workspace_region", "measure_copy", "measure_mfma",
+           "HagdnError"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.path.join(_HERE, "libhagdn.so")
@@ -66,7 +67,15 @@ _SYMBOLS = {
     "hagdn_version": (ctypes.c_int, []),
     "hagdn_set_segment_chunks": (ctypes.c_int, [ctypes.c_int]),
     "hagdn_segment_chunks": (ctypes.c_int, [ctypes.c_int] * 6),
+    "hagdn_segment_chunks_for": (ctypes.c_int, [ctypes.c_int] * 7),
+    "hagdn_workspace_region": (ctypes.c_int, [ctypes.c_int] * 9 + [ctypes.POINTER(ctypes.c_size_t)] * 2),
+    "hagdn_measure_copy": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "hagdn_measure_mfma": (ctypes.c_int, [ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t,
+                                          ctypes.POINTER(ctypes.c_double), ctypes.c_void_p]),
 }
+
+# workspace regions (hagdn_ws_region)
+WS_NM, WS_B, WS_QP, WS_OLOC, WS_DECAY, WS_SEG_A, WS_SEG_B = range(7)
 
 
 class HagdnError(RuntimeError):
@@ -127,12 +136,27 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _check_buffer(name, t, device, dtype, shape):
+    """A caller-supplied buffer the kernels write or read through a raw pointer:
+    on the call's GPU, of the expected dtype, shape and contiguous layout."""
+    if not t.is_cuda or t.device != device:
+        raise ValueError(f"{name} must be on {device} (got {t.device})")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
 def _prefill(kind, q, k, v, g, beta, initial_state, cu_seqlens, scale, output_final_state,
              workspace, out, final_out, preprocess=0):
     import torch
     lib = load_library()
     if not (q.is_cuda and k.is_cuda and v.is_cuda and g.is_cuda and beta.is_cuda):
         raise ValueError("all tensors must be on the GPU")
+    if not all(t.device == q.device for t in (k, v, g, beta)):
+        raise ValueError("q, k, v, g and beta must be on one device")
     if not (q.dtype == k.dtype == v.dtype):
         raise TypeError("q, k, v must share one dtype")
     dt = _dtype_code(q.dtype)
@@ -153,19 +177,26 @@ def _prefill(kind, q, k, v, g, beta, initial_state, cu_seqlens, scale, output_fi
         cu_seqlens = torch.tensor([0, T], dtype=torch.int32, device=dev)
     if cu_seqlens.dtype != torch.int32 or not cu_seqlens.is_cuda or not cu_seqlens.is_contiguous():
         raise TypeError("cu_seqlens must be a contiguous int32 GPU tensor")
+    if cu_seqlens.device != dev or cu_seqlens.dim() != 1:
+        raise ValueError(f"cu_seqlens must be a 1-D tensor on {dev}")
     N = cu_seqlens.shape[0] - 1
+    state_shape = (N, Hv, Dk, Dv)
     if initial_state is not None:
-        if initial_state.dtype != torch.float32 or tuple(initial_state.shape) != (N, Hv, Dk, Dv) \
-                or not initial_state.is_contiguous():
-            raise ValueError(f"initial_state must be contiguous float32 {(N, Hv, Dk, Dv)}")
+        _check_buffer("initial_state", initial_state, dev, torch.float32, state_shape)
+    if out is not None:
+        _check_buffer("out", out, dev, q.dtype, (T, Hv, Dv))
     o = out if out is not None else torch.empty((T, Hv, Dv), dtype=q.dtype, device=dev)
     sf = None
     if output_final_state:
-        sf = final_out if final_out is not None else torch.empty((N, Hv, Dk, Dv),
-                                                                 dtype=torch.float32, device=dev)
+        if final_out is not None:
+            _check_buffer("final_out", final_out, dev, torch.float32, state_shape)
+        sf = final_out if final_out is not None else torch.empty(state_shape, dtype=torch.float32,
+                                                                 device=dev)
     need = workspace_size(kind, N, T, Hqk, Hv, Dk, Dv, dt)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    elif not workspace.is_cuda or workspace.device != dev or not workspace.is_contiguous():
+        raise ValueError(f"workspace must be a contiguous tensor on {dev}")
     stream = torch.cuda.current_stream(dev).cuda_stream
     fn = lib.gdn_prefill_ex if kind == "gdn" else lib.kda_prefill_ex
     rc = fn(_ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta), _ptr(initial_state), _ptr(cu_seqlens),
@@ -197,8 +228,8 @@ def _decode(kind, q, k, v, g, beta, state, slots, scale, preprocess, out):
     import torch
     lib = load_library()
     for name, t in (("q", q), ("k", k), ("v", v), ("g", g), ("beta", beta), ("state", state)):
-        if not t.is_cuda or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous GPU tensor")
+        if not t.is_cuda or not t.is_contiguous() or t.device != q.device:
+            raise ValueError(f"{name} must be a contiguous tensor on {q.device}")
     if not (q.dtype == k.dtype == v.dtype):
         raise TypeError("q, k, v must share one dtype")
     dt = _dtype_code(q.dtype)
@@ -217,8 +248,10 @@ def _decode(kind, q, k, v, g, beta, state, slots, scale, preprocess, out):
         if state.shape[0] < N:
             raise ValueError("without slots the state pool needs one state per sequence")
     elif slots.dtype != torch.int32 or not slots.is_cuda or tuple(slots.shape) != (N,) \
-            or not slots.is_contiguous():
-        raise TypeError("slots must be a contiguous int32 GPU tensor of length N")
+            or not slots.is_contiguous() or slots.device != q.device:
+        raise TypeError(f"slots must be a contiguous int32 tensor of length N on {q.device}")
+    if out is not None:
+        _check_buffer("out", out, q.device, q.dtype, (N, Hv, Dv))
     o = out if out is not None else torch.empty((N, Hv, Dv), dtype=q.dtype, device=q.device)
     stream = torch.cuda.current_stream(q.device).cuda_stream
     fn = lib.gdn_decode if kind == "gdn" else lib.kda_decode
@@ -275,6 +308,60 @@ def segment_chunks(N: int, T: int, Hv: int, Dv: int, dtype=None, kind: str = "gd
     if kind not in ("gdn", "kda"):
         raise ValueError(f"kind must be 'gdn' or 'kda', not {kind!r}")
     L = lib.hagdn_segment_chunks(int(N), int(T), int(Hv), int(Dv), code, int(kind == "kda"))
+    if L < 0:
+        raise HagdnError(1, _err(lib))
+    return L
+
+
+def workspace_region(kind, N, T, Hqk, Hv, Dk, Dv, dtype_code, region):
+    """(byte offset, bytes) of a workspace region (WS_*) for a call with these sizes."""
+    lib = load_library()
+    off, n = ctypes.c_size_t(), ctypes.c_size_t()
+    rc = lib.hagdn_workspace_region(int(kind == "kda"), N, T, Hqk, Hv, Dk, Dv, dtype_code, int(region),
+                                    ctypes.byref(off), ctypes.byref(n))
+    if rc != 0:
+        raise HagdnError(rc, _err(lib))
+    return off.value, n.value
+
+
+def measure_copy(src, dst):
+    """Enqueue the library's streaming copy of src into dst (same byte size) on
+    torch's current stream."""
+    import torch
+    lib = load_library()
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != n or not (src.is_cuda and dst.is_cuda):
+        raise ValueError("src and dst must be GPU tensors of one byte size")
+    rc = lib.hagdn_measure_copy(_ptr(src), _ptr(dst), n,
+                                ctypes.c_void_p(torch.cuda.current_stream(src.device).cuda_stream))
+    if rc != 0:
+        raise HagdnError(rc, _err(lib))
+
+
+def measure_mfma(iterations, sink):
+    """Enqueue the library's bf16 MFMA loop on torch's current stream; returns
+    the FLOPs it performs.  sink: a float32 GPU tensor of >= 16 x CUs elements."""
+    import torch
+    lib = load_library()
+    flops = ctypes.c_double()
+    rc = lib.hagdn_measure_mfma(int(iterations), _ptr(sink), sink.numel(), ctypes.byref(flops),
+                                ctypes.c_void_p(torch.cuda.current_stream(sink.device).cuda_stream))
+    if rc != 0:
+        raise HagdnError(rc, _err(lib))
+    return flops.value
+
+
+def segment_chunks_for(N: int, T: int, Hv: int, Dv: int, cus: int, dtype=None,
+                       kind: str = "gdn") -> int:
+    """The automatic segment length for a device of ``cus`` compute units (host
+    rule only, no device query; a forced length applies here too)."""
+    import torch
+    lib = load_library()
+    code = _dtype_code(torch.bfloat16 if dtype is None else dtype)
+    if kind not in ("gdn", "kda"):
+        raise ValueError(f"kind must be 'gdn' or 'kda', not {kind!r}")
+    L = lib.hagdn_segment_chunks_for(int(N), int(T), int(Hv), int(Dv), code, int(kind == "kda"),
+                                     int(cus))
     if L < 0:
         raise HagdnError(1, _err(lib))
     return L

@@ -53,35 +53,63 @@ constexpr int kDecodeKernel = 4;
 // Chunks per segment of the state chain; 0 = chosen per call (seg_chunks).
 std::atomic<int> g_seg_override{0};
 constexpr int kMaxSegChunks = 1 << 20;
-constexpr long kCus = 256;  // compute units of an MI355X (gfx950)
+// Compute units assumed by the size and segment-length queries when no HIP
+// device can be queried (a host without a GPU: nothing can launch there, the
+// answers only describe an MI355X).  Calls that launch always query.
+constexpr int kNoDeviceCus = 256;
 
-// Segment length for a batch of N sequences over T tokens.  A chain of n
-// chunks walked whole costs n dependent steps; its workgroups (one per
-// sequence, value head and 16-column tile) occupy N Hv Dv/16 CUs.  Cut into
-// segments of L, it costs about L steps for the segment maps, n / L for the
-// prefix and L for the walk, each step about three times as long (one
-// head-resident workgroup moves a whole head's operands through one CU), on
-// about (n / L) Hv workgroups.  Measured on MI355X (1 sequence, d = 128, bf16,
-// operator totals): with 16 heads (128 walk workgroups) segments pay from
-// about 120 chunks (T = 6144: 135 us whole against 141 at L = 12; T = 8192:
-// 187 against 182 at L = 12; T = 9216: 235 against 200; T = 12288: 341
-// against 267), and the best L puts about one segment workgroup on every CU
-// (L = n Hv / 256, at least 12).  With 32 heads (256 walk workgroups) the
-// whole walk still won at 256 chunks (T = 16384: 596 us against 619 at
-// L = 32; 192 chunks: 484 against 480), so the threshold grows with the
-// walks' share of the CUs, r = walks / 128: 120 r + 48 (r - 1) chunks.  KDA pays from fewer chunks: its
-// per-channel gate adds 8 KiB per token (d = 128) to the chunk-local kernel's
-// input and pushes the walk's operands out of the Infinity Cache sooner.  With
-// 16 heads: T = 4096 128 us whole against 132 at L = 8; T = 6144 180 against
-// 176 at L = 8; T = 8192 251 against 217.  KDA segments from 88 chunks with L
-// at least 8.
+// Compute units of the current device, queried once per device (0 if the
+// query fails).  Both the segment rule and the choice of walk kernel use it.
+int current_device_cus() {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> cache[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  int n = dev >= 0 && dev < kMaxDevices ? cache[dev].load(std::memory_order_relaxed) : 0;
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) return 0;
+    if (dev >= 0 && dev < kMaxDevices) cache[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+int query_cus() {
+  const int n = current_device_cus();
+  return n > 0 ? n : kNoDeviceCus;
+}
+
+// Segment length for a batch of N sequences over T tokens on a device of
+// `cus` compute units.  A chain of n chunks walked whole costs n dependent
+// steps; its workgroups (one per sequence, value head and 16-column tile)
+// occupy N Hv Dv/16 CUs.  Cut into segments of L, it costs about L steps for
+// the segment maps, n / L for the prefix and L for the walk, each step about
+// three times as long (one head-resident workgroup moves a whole head's
+// operands through one CU), on about (n / L) Hv workgroups.
+//
+// The thresholds come from sweeps of single sequences on an MI355X (256 CUs;
+// d = 128, bf16, operator totals in us, whole chain against the best L):
+//   GDN, 16 heads (128 walk workgroups, half the CUs): T = 6144 (96 chunks)
+//     135 against 141 (L = 12); 7168 (112) 162 against 161 (L = 8); 8192
+//     (128) 185 against 176 (L = 12); 9216 235 against 200; 12288 341
+//     against 267.  Segments pay from about 120 chunks, and the best L puts
+//     about one segment workgroup on every CU: L = n Hv / cus, at least 12.
+//   GDN, 32 heads (256 walk workgroups, every CU): 192 chunks 484 against
+//     480 (L = 24), 256 chunks 596 against 619 (L = 32): the whole walk holds
+//     longer, so the threshold grows with the walks' share of the CUs,
+//     r = walks / (cus / 2): 120 r + 48 (r - 1) chunks.
+//   KDA, 16 heads: T = 4096 128 against 132 (L = 8); 6144 180 against 176
+//     (L = 8); 8192 251 against 217.  Its per-channel gate adds 8 KiB per
+//     token (d = 128) to the chunk-local kernel's input and pushes the walk's
+//     operands out of the Infinity Cache sooner: KDA segments from 88 r +
+//     48 (r - 1) chunks with L at least 8.
+// Both scale with the CU count only through r and L = n Hv / cus; a device
+// with fewer CUs (a partition) segments earlier and with longer segments.
 //
 // Whatever the choice (or override), L is capped so that the o rows of one
 // segment, 64 L Hv Dv elements, span less than 2 GiB: the walk kernels address
 // a segment's rows through one buffer resource with 32-bit signed byte
 // offsets.  A call whose chains do not fit one capped segment takes the
 // segmented path, whose windows then fit too.
-int seg_chunks(int N, int T, int Hv, int Dv, size_t esz, bool kda) {
+int seg_chunks(int N, int T, int Hv, int Dv, size_t esz, bool kda, int cus) {
   const size_t seg_rows_bytes = (size_t)hagdn::kChunk * (size_t)Hv * (size_t)Dv * esz;
   const long cap = std::max<long>(1, (long)(((size_t)1 << 31) - 1) / (long)seg_rows_bytes);
   const int ov = g_seg_override.load(std::memory_order_relaxed);
@@ -92,10 +120,11 @@ int seg_chunks(int N, int T, int Hv, int Dv, size_t esz, bool kda) {
     const long n_all = ((long)T + hagdn::kChunk - 1) / hagdn::kChunk;  // longest possible chain
     const long n_avg = ((long)T / (N > 0 ? N : 1) + hagdn::kChunk - 1) / hagdn::kChunk;
     const double walks = (double)(N > 0 ? N : 1) * Hv * std::max(1, Dv / 16);
-    const double r = std::max(1.0, walks / (kCus / 2));
+    const long c = std::max(2, cus);
+    const double r = std::max(1.0, walks / (double)(c / 2));
     const double threshold = (kda ? 88.0 : 120.0) * r + 48.0 * (r - 1.0);
     if ((double)n_avg < threshold) L = n_all > 0 ? std::min<long>(n_all, kMaxSegChunks) : 1;
-    else L = std::max<long>(kda ? 8 : 12, (n_all * Hv + kCus - 1) / kCus);
+    else L = std::max<long>(kda ? 8 : 12, (n_all * Hv + c - 1) / c);
   }
   return (int)std::min(L, cap);
 }
@@ -105,19 +134,19 @@ bool add_ok(size_t a, size_t b, size_t *out) { return !__builtin_add_overflow(a,
 
 // Byte offsets of every workspace region (each 256-byte aligned).
 struct Layout {
-  size_t status, seq_info, chunk_info, NM, Bc, Qp, Ol, dec, seq_seg, seg_info, Aseg, Bseg, total;
+  size_t status, seq_info, chunk_info, NM, Bc, Qp, Ol, dec, seq_seg, seg_info, Aseg, Bseg, s0c, total;
   int max_chunks, seg_chunks, max_segs;
 };
 
 // Returns false (with the error set) if the sizes overflow.
-bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, bool kda, Layout *L) {
+bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, bool kda, int cus, Layout *L) {
   const size_t mc = (size_t)(T / hagdn::kChunk) + (size_t)N;
   if (mc > 0x7fffffffu) {
     fail(HAGDN_EINVAL, "too many chunks (%zu)", mc);
     return false;
   }
   L->max_chunks = (int)mc;
-  L->seg_chunks = seg_chunks(N, T, Hv, Dv, esz, kda);
+  L->seg_chunks = seg_chunks(N, T, Hv, Dv, esz, kda, cus);
   const size_t ms = mc / (size_t)L->seg_chunks + (size_t)N;
   L->max_segs = (int)ms;  // <= mc
   size_t blocks, sblocks;  // (chunk, value head) and (segment, value head) blocks
@@ -149,6 +178,7 @@ bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, bool kda, Lay
   const bool maps = (size_t)(T + hagdn::kChunk - 1) / hagdn::kChunk > (size_t)L->seg_chunks;
   L->Aseg = region((size_t)Dk * Dk, esz, maps ? sblocks : 0);
   L->Bseg = region((size_t)Dk * Dv, sizeof(float), maps ? sblocks : 0);
+  L->s0c = region((size_t)Dk * Dv, sizeof(float), maps ? (size_t)N * (size_t)Hv : 0);
   L->total = (off + kAlign - 1) / kAlign * kAlign;
   if (!ok) fail(HAGDN_EINVAL, "workspace size overflows");
   return ok;
@@ -170,7 +200,7 @@ int check_shapes(int N, int T, int Hqk, int Hv, int Dk, int Dv, int dtype) {
 size_t workspace_size(bool kda, int N, int T, int Hqk, int Hv, int Dk, int Dv, int dtype) {
   if (check_shapes(N, T, Hqk, Hv, Dk, Dv, dtype) != HAGDN_OK) return 0;
   Layout L;
-  if (!make_layout(N, T, Hv, Dk, Dv, dtype == HAGDN_BF16 ? 2 : 4, kda, &L)) return 0;
+  if (!make_layout(N, T, Hv, Dk, Dv, dtype == HAGDN_BF16 ? 2 : 4, kda, query_cus(), &L)) return 0;
   return L.total;
 }
 
@@ -218,8 +248,9 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
     if (a0 < a1 + sb && a1 < a0 + sb) return fail(HAGDN_EINVAL, "s_final overlaps s0 without aliasing it exactly");
   }
   const bool bf16 = dtype == HAGDN_BF16;
+  const int cus = query_cus();  // the workspace-size query's answer for this device
   Layout L;
-  if (!make_layout(N, T, Hv, Dk, Dv, bf16 ? 2 : 4, kda, &L)) return HAGDN_EINVAL;
+  if (!make_layout(N, T, Hv, Dk, Dv, bf16 ? 2 : 4, kda, cus, &L)) return HAGDN_EINVAL;
   if (ws_bytes < L.total)
     return fail(HAGDN_EWORKSPACE, "workspace too small: %zu bytes given, %zu needed", ws_bytes, L.total);
 
@@ -242,7 +273,9 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   a.seg_info = reinterpret_cast<int4 *>(w + L.seg_info);
   a.Aseg = w + L.Aseg;
   a.Bseg = reinterpret_cast<float *>(w + L.Bseg);
+  a.s0c = reinterpret_cast<float *>(w + L.s0c);
   a.single = N == 1 ? 1 : 0;  // the kernels derive a single sequence's tables themselves
+  a.cus = cus;
   const bool maps = (T + hagdn::kChunk - 1) / hagdn::kChunk > L.seg_chunks;
 
   hipStream_t st = static_cast<hipStream_t>(stream_);
@@ -456,11 +489,66 @@ int hagdn_set_segment_chunks(int chunks) {
   return HAGDN_OK;
 }
 
-int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv, int dtype, int kda) {
+int hagdn_measure_copy(const void *src, void *dst, size_t bytes, void *stream) {
+  if (!src || !dst) return fail(HAGDN_EINVAL, "NULL src or dst");
+  if (bytes % 16 || !aligned(src, 16) || !aligned(dst, 16))
+    return fail(HAGDN_EINVAL, "copy needs 16-byte aligned buffers and a multiple of 16 bytes");
+  const char *a = static_cast<const char *>(src), *b = static_cast<const char *>(dst);
+  if (a < b + bytes && b < a + bytes) return fail(HAGDN_EINVAL, "src and dst overlap");
+  if (bytes == 0) return HAGDN_OK;
+  hipError_t e = hagdn::launch_copy(src, dst, bytes, current_device_cus(), static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? HAGDN_OK : fail(HAGDN_EHIP, "HIP error: %s", hipGetErrorString(e));
+}
+
+int hagdn_measure_mfma(int iterations, float *sink, size_t sink_floats, double *flops, void *stream) {
+  if (!sink || !flops) return fail(HAGDN_EINVAL, "NULL sink or flops");
+  if (iterations < 1 || iterations > (1 << 24)) return fail(HAGDN_EINVAL, "iterations out of range [1, 2^24]");
+  const int cus = current_device_cus();
+  if (cus <= 0) return fail(HAGDN_EHIP, "cannot query the current HIP device");
+  const int blocks = 4 * cus;  // four waves per workgroup: 16 waves per CU, 4 per SIMD
+  if (sink_floats < (size_t)blocks * 4)
+    return fail(HAGDN_EINVAL, "sink needs %d floats (4 per workgroup of 4 x CUs)", blocks * 4);
+  if (!aligned(sink, 4)) return fail(HAGDN_EINVAL, "sink must be 4-byte aligned");
+  hipError_t e = hagdn::launch_mfma_loop(blocks, iterations, sink, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(HAGDN_EHIP, "HIP error: %s", hipGetErrorString(e));
+  *flops = 2.0 * 16 * 16 * 32 * 8 * (double)iterations * blocks * 4;
+  return HAGDN_OK;
+}
+
+int hagdn_workspace_region(int kda, int N, int T_total, int Hqk, int Hv, int Dk, int Dv, int dtype,
+                           int region, size_t *offset, size_t *bytes) {
+  if (!offset || !bytes) return fail(HAGDN_EINVAL, "NULL offset or bytes");
+  int rc = check_shapes(N, T_total, Hqk, Hv, Dk, Dv, dtype);
+  if (rc != HAGDN_OK) return rc;
+  Layout L;
+  if (!make_layout(N, T_total, Hv, Dk, Dv, dtype == HAGDN_BF16 ? 2 : 4, kda != 0, query_cus(), &L))
+    return HAGDN_EINVAL;
+  size_t at, next;
+  switch (region) {
+    case HAGDN_WS_NM: at = L.NM; next = L.Bc; break;
+    case HAGDN_WS_B: at = L.Bc; next = L.Qp; break;
+    case HAGDN_WS_QP: at = L.Qp; next = L.Ol; break;
+    case HAGDN_WS_OLOC: at = L.Ol; next = L.dec; break;
+    case HAGDN_WS_DECAY: at = L.dec; next = L.seq_seg; break;
+    case HAGDN_WS_SEG_A: at = L.Aseg; next = L.Bseg; break;
+    case HAGDN_WS_SEG_B: at = L.Bseg; next = L.s0c; break;
+    default: return fail(HAGDN_EINVAL, "unknown workspace region %d", region);
+  }
+  *offset = at;
+  *bytes = next - at;  // the region plus its alignment padding
+  return HAGDN_OK;
+}
+
+int hagdn_segment_chunks_for(int N, int T_total, int Hv, int Dv, int dtype, int kda, int cus) {
   if (N < 1 || T_total < 0 || Hv < 1 || Dv < 1)
     return fail(HAGDN_EINVAL, "bad shape"), -1;
   if (dtype != HAGDN_F32 && dtype != HAGDN_BF16) return fail(HAGDN_EINVAL, "bad dtype %d", dtype), -1;
-  return seg_chunks(N, T_total, Hv, Dv, dtype == HAGDN_BF16 ? 2 : 4, kda != 0);
+  if (cus < 1) return fail(HAGDN_EINVAL, "compute units must be >= 1 (got %d)", cus), -1;
+  return seg_chunks(N, T_total, Hv, Dv, dtype == HAGDN_BF16 ? 2 : 4, kda != 0, cus);
+}
+
+int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv, int dtype, int kda) {
+  return hagdn_segment_chunks_for(N, T_total, Hv, Dv, dtype, kda, query_cus());
 }
 
 }  // extern "C"

@@ -91,7 +91,9 @@ struct LocalLayout {
   static constexpr size_t off_beta = off_Vt + sizeof(T) * DV * kChunk;                // GDN
   static constexpr size_t off_kdec = off_beta + (KDA ? 0 : sizeof(float) * kChunk);   // GDN
   static constexpr size_t off_gam = off_kdec + (KDA ? 0 : sizeof(float) * kChunk);
-  static constexpr size_t bytes = off_gam + sizeof(float) * kChunk * (KDA ? DK : 1);
+  // GDN: the scalar gate scan in fp64 (gamma reaches thousands in magnitude
+  // where gates are near 0, and the decays are exponentials of differences)
+  static constexpr size_t bytes = off_gam + (KDA ? sizeof(float) * kChunk * DK : sizeof(double) * kChunk);
   // KDA gate-scan segment totals: kLocalThreads floats in region Y, behind the
   // kLocalThreads-float scratch of the q/k normalisation
   static constexpr size_t off_tot = off_A + sizeof(float) * kLocalThreads;
@@ -300,7 +302,8 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
   float *sBeta = reinterpret_cast<float *>(smem + L::off_beta);
   float *sKdec = reinterpret_cast<float *>(smem + L::off_kdec);
   float *sTot = reinterpret_cast<float *>(smem + L::off_tot);
-  float *sGam = reinterpret_cast<float *>(smem + L::off_gam);
+  float *sGam = reinterpret_cast<float *>(smem + L::off_gam);     // KDA: [64][DK] (gam_at)
+  double *sGd = reinterpret_cast<double *>(smem + L::off_gam);    // GDN: [64], fp64
   T *sWt = reinterpret_cast<T *>(smem + L::off_A);  // region Y once every wave holds its T rows
   T *sUt = sVt;  // region Z once op #4 has read the values
 
@@ -340,13 +343,13 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
   }
   if constexpr (!KDA) {
     if (wave == 0) {
-      float x = gk[0];
+      double x = gk[0];
 #pragma unroll
       for (int off = 1; off < 64; off <<= 1) {
-        const float y = __shfl_up(x, off);
+        const double y = __shfl_up(x, off);
         if (lane >= off) x += y;
       }
-      sGam[lane] = x;
+      sGd[lane] = x;
     }
   } else {
     // segment-local scan in registers, then add the totals of earlier segments
@@ -393,7 +396,7 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int s = 16 * j + 4 * grp + e;
-          const float dec = s <= r ? __expf(sGam[r] - sGam[s]) : 0.f;
+          const float dec = s <= r ? __expf((float)(sGd[r] - sGd[s])) : 0.f;
           accA[j][e] = s < r ? sBeta[r] * accA[j][e] * dec : 0.f;
           accP[j][e] = accP[j][e] * dec * qscale;
         }
@@ -403,44 +406,136 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
       // Per-channel decay e^(gamma_r - gamma_s), factored around a reference
       // token rho in the middle of this wave's block: the r side carries
       // e^(gamma_r - gamma_rho), the s side e^(gamma_rho - gamma_s), so every
-      // block -- the diagonal one included -- is an MFMA product.  Each factor
-      // spans at most 8 tokens of decay inside the block (|exponent| <= 8 max g,
-      // far from fp32/bf16 overflow); off-diagonal s-side factors are <= 1.
-      // Upper-triangle products of the diagonal block may overflow: they are
-      // discarded by selection below, never multiplied.
+      // block -- the diagonal one included -- is an MFMA product.  Inside the
+      // block each factor spans at most 8 tokens of decay; off-diagonal s-side
+      // factors are <= 1.  Upper-triangle products of the diagonal block may
+      // overflow: they are discarded by selection below, never multiplied.
+      //
+      // This is exact up to rounding while every exponent of the block stays
+      // within +-kFactorExp (kFactorExp < 88, the fp32/bf16 overflow point):
+      // no factor overflows, and an s-side factor that underflows belongs to
+      // a product below e^(kFactorExp - 87), far under any rounding error.  A
+      // block in which some channel decays by more than e^kFactorExp over
+      // half a block (a strongly forgetting channel: a gate near 0 for a few
+      // tokens) takes the exact path instead: off-diagonal blocks factored
+      // around the last token of the s block (both factors <= 1), the diagonal
+      // block elementwise.  The choice is per wave (one row block), uniform.
+      constexpr float kFactorExp = 40.f;
       const int rho = 16 * i + 8;
-      // B operands (token r side): k_r e^(gamma_r - gamma_rho), q_r e^(gamma_r - gamma_rho)
-      Frag<T> kr[DK / 32], qr[DK / 32];
+      bool wide = false;
 #pragma unroll
       for (int kb = 0; kb < DK / 32; ++kb) {
-        float xk[8], xq[8], gr[8], gh[8];
-        const Frag<T> kraw = frag_sw<L::LDK>(sK, r, kb * 32 + 8 * grp);  // channels kc(grp, 0..7)
+        float gr[8], gh[8];
         gam8<DK>(sGam, r, kb * 32 + kc(grp, 0), gr);
         gam8<DK>(sGam, rho, kb * 32 + kc(grp, 0), gh);
 #pragma unroll
-        for (int jj = 0; jj < 8; ++jj) {
-          const float ex = __expf(gr[jj] - gh[jj]);
-          xk[jj] = frag_elem(kraw, jj) * ex;
-          xq[jj] = frag_elem(qf[kb], jj) * ex;
-        }
-        kr[kb] = make_frag<T>(xk);
-        qr[kb] = make_frag<T>(xq);
+        for (int jj = 0; jj < 8; ++jj) wide |= fabsf(gr[jj] - gh[jj]) > kFactorExp;
       }
+      if (!__builtin_amdgcn_ballot_w64(wide)) {
+        // B operands (token r side): k_r e^(gamma_r - gamma_rho), q_r e^(gamma_r - gamma_rho)
+        Frag<T> kr[DK / 32], qr[DK / 32];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (j <= i) {  // uniform for the wave
-          const int sb = 16 * j + col;
+        for (int kb = 0; kb < DK / 32; ++kb) {
+          float xk[8], xq[8], gr[8], gh[8];
+          const Frag<T> kraw = frag_sw<L::LDK>(sK, r, kb * 32 + 8 * grp);  // channels kc(grp, 0..7)
+          gam8<DK>(sGam, r, kb * 32 + kc(grp, 0), gr);
+          gam8<DK>(sGam, rho, kb * 32 + kc(grp, 0), gh);
+#pragma unroll
+          for (int jj = 0; jj < 8; ++jj) {
+            const float ex = __expf(gr[jj] - gh[jj]);
+            xk[jj] = frag_elem(kraw, jj) * ex;
+            xq[jj] = frag_elem(qf[kb], jj) * ex;
+          }
+          kr[kb] = make_frag<T>(xk);
+          qr[kb] = make_frag<T>(xq);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (j <= i) {  // uniform for the wave
+            const int sb = 16 * j + col;
+#pragma unroll
+            for (int kb = 0; kb < DK / 32; ++kb) {
+              float xs[8], gh[8], gs[8];
+              const Frag<T> sraw = frag_sw<L::LDK>(sK, sb, kb * 32 + 8 * grp);
+              gam8<DK>(sGam, rho, kb * 32 + kc(grp, 0), gh);
+              gam8<DK>(sGam, sb, kb * 32 + kc(grp, 0), gs);
+#pragma unroll
+              for (int jj = 0; jj < 8; ++jj) xs[jj] = frag_elem(sraw, jj) * __expf(gh[jj] - gs[jj]);
+              const Frag<T> ks = make_frag<T>(xs);
+              accA[j] = mma(accA[j], ks, kr[kb]);
+              accP[j] = mma(accP[j], ks, qr[kb]);
+            }
+          }
+        }
+      } else {
+        // off-diagonal blocks j < i around the last token e of block j:
+        // e^(gamma_r - gamma_e) <= 1 (r > e) and e^(gamma_e - gamma_s) <= 1 (s <= e)
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+          if (j < i) {  // uniform for the wave
+            const int e = 16 * j + 15, sb = 16 * j + col;
+#pragma unroll
+            for (int kb = 0; kb < DK / 32; ++kb) {
+              float xk[8], xq[8], xs[8], gr[8], ge[8], gs[8];
+              const Frag<T> kraw = frag_sw<L::LDK>(sK, r, kb * 32 + 8 * grp);
+              const Frag<T> sraw = frag_sw<L::LDK>(sK, sb, kb * 32 + 8 * grp);
+              gam8<DK>(sGam, r, kb * 32 + kc(grp, 0), gr);
+              gam8<DK>(sGam, e, kb * 32 + kc(grp, 0), ge);
+              gam8<DK>(sGam, sb, kb * 32 + kc(grp, 0), gs);
+#pragma unroll
+              for (int jj = 0; jj < 8; ++jj) {
+                const float fr = __expf(gr[jj] - ge[jj]);
+                xk[jj] = frag_elem(kraw, jj) * fr;
+                xq[jj] = frag_elem(qf[kb], jj) * fr;
+                xs[jj] = frag_elem(sraw, jj) * __expf(ge[jj] - gs[jj]);
+              }
+              const Frag<T> ks = make_frag<T>(xs);
+              accA[j] = mma(accA[j], ks, make_frag<T>(xk));
+              accP[j] = mma(accP[j], ks, make_frag<T>(xq));
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          }
+        }
+        // diagonal block elementwise in fp32, one token s = 16i + sl at a time:
+        // lane (col, grp) sums its 32 channels for token r = 16i + col (with
+        // e^min(gamma_r - gamma_s, 0): upper-triangle terms, s > r, are
+        // discarded below), the four lane groups of a column add up, and the
+        // lane group that holds accumulator row s keeps the sum
+        f32x4 va = zero4(), vp = zero4();
+#pragma unroll 1
+        for (int sl = 0; sl < 16; ++sl) {
+          float sa = 0.f, sp = 0.f;
 #pragma unroll
           for (int kb = 0; kb < DK / 32; ++kb) {
-            float xs[8], gh[8], gs[8];
-            const Frag<T> sraw = frag_sw<L::LDK>(sK, sb, kb * 32 + 8 * grp);
-            gam8<DK>(sGam, rho, kb * 32 + kc(grp, 0), gh);
-            gam8<DK>(sGam, sb, kb * 32 + kc(grp, 0), gs);
+            float gr[8], gs[8];
+            const Frag<T> kraw = frag_sw<L::LDK>(sK, r, kb * 32 + 8 * grp);
+            const Frag<T> sraw = frag_sw<L::LDK>(sK, 16 * i + sl, kb * 32 + 8 * grp);
+            gam8<DK>(sGam, r, kb * 32 + kc(grp, 0), gr);
+            gam8<DK>(sGam, 16 * i + sl, kb * 32 + kc(grp, 0), gs);
 #pragma unroll
-            for (int jj = 0; jj < 8; ++jj) xs[jj] = frag_elem(sraw, jj) * __expf(gh[jj] - gs[jj]);
-            const Frag<T> ks = make_frag<T>(xs);
-            accA[j] = mma(accA[j], ks, kr[kb]);
-            accP[j] = mma(accP[j], ks, qr[kb]);
+            for (int jj = 0; jj < 8; ++jj) {
+              const float t = frag_elem(sraw, jj) * __expf(fminf(gr[jj] - gs[jj], 0.f));
+              sa += frag_elem(kraw, jj) * t;
+              sp += frag_elem(qf[kb], jj) * t;
+            }
+            __builtin_amdgcn_sched_barrier(0);  // one k-block of operands in registers at a time
+          }
+          sa += __shfl_xor(sa, 16);
+          sa += __shfl_xor(sa, 32);
+          sp += __shfl_xor(sp, 16);
+          sp += __shfl_xor(sp, 32);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bool mine = 4 * grp + e == sl;
+            va[e] = mine ? sa : va[e];
+            vp[e] = mine ? sp : vp[e];
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (j == i) {  // uniform for the wave
+            accA[j] = va;
+            accP[j] = vp;
           }
         }
       }
@@ -536,7 +631,7 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
   {
     const int i = wave, r = 16 * i + col;
     if constexpr (!KDA) {
-      if (tid < kChunk) sKdec[tid] = __expf(sGam[kChunk - 1] - sGam[tid]);
+      if (tid < kChunk) sKdec[tid] = __expf((float)(sGd[kChunk - 1] - sGd[tid]));
     }
     Frag<T> tu[2], tw[2];
 #pragma unroll
@@ -548,7 +643,7 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
         const int s = kb * 32 + kc(grp, j);
         const float t = trow[j] * (KDA ? bs[kb][j] : sBeta[s]);
         xu[j] = t;
-        xw[j] = KDA ? t : t * __expf(sGam[s]);
+        xw[j] = KDA ? t : t * __expf((float)sGd[s]);
       }
       tu[kb] = make_frag<T>(xu);
       tw[kb] = make_frag<T>(xw);
@@ -616,7 +711,7 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
     if constexpr (KDA) {
       if (tid < DK) dec_out[tid] = __expf(sGam[gam_at<DK>(kChunk - 1, tid)]);
     } else {
-      if (tid == 0) dec_out[0] = __expf(sGam[kChunk - 1]);
+      if (tid == 0) dec_out[0] = __expf((float)sGd[kChunk - 1]);
     }
   }
   __syncthreads();
@@ -702,7 +797,7 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
         for (int kb = 0; kb < 2; ++kb)
           if (kb < nkb) acc = mma(acc, frag_sw<L::LDT>(sWt, 16 * m + col, kb * 32 + 8 * grp), pb[kb]);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) qe[e] *= KDA ? __expf(gq[e]) : __expf(sGam[r]);
+        for (int e = 0; e < 4; ++e) qe[e] *= KDA ? __expf(gq[e]) : __expf((float)sGd[r]);
         res[h] = qe - acc;
       }
       // slots 4(m & 1) + e of block kb = m >> 1: m2 and m2 + 1 fill them, one 16-byte store

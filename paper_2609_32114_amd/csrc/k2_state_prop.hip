@@ -44,8 +44,6 @@
 // all d_v tiles of one (sequence, head) pair get ids in one such class and
 // share that XCD's L2 for NM, which every tile of the pair reads.
 
-#include <atomic>
-
 #include "device.h"
 #include "prefill.h"
 
@@ -286,22 +284,6 @@ __global__ __launch_bounds__(64 * (DK / 32), sizeof(T) == 2 ? 2 : 1) void state_
   }
 }
 
-// CUs of the current device, looked up once per device.
-static hipError_t device_cus(int *out) {
-  constexpr int kMaxDevices = 64;
-  static std::atomic<int> cache[kMaxDevices];
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  int n = dev >= 0 && dev < kMaxDevices ? cache[dev].load(std::memory_order_relaxed) : 0;
-  if (n == 0) {
-    if ((e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
-    if (dev >= 0 && dev < kMaxDevices) cache[dev].store(n, std::memory_order_relaxed);
-  }
-  *out = n;
-  return hipSuccess;
-}
-
 template <typename T, int DK, int DV, bool KDA>
 static hipError_t launch_state_t(const PrefillArgs &a, hipStream_t stream) {
   const long pairs = (long)a.N * a.Hv;
@@ -327,11 +309,8 @@ static hipError_t dispatch_dims(const PrefillArgs &a, hipStream_t s) {
 hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStream_t s) {
   if (bf16) {
     // more walks than CUs: the staged walk, several tiles per workgroup
-    int cus = 0;
-    hipError_t e = device_cus(&cus);
-    if (e != hipSuccess) return e;
     const long walks = ((long)a.N * a.Hv + kXcds - 1) / kXcds * kXcds * (a.Dv / 16);
-    if (walks > cus) return launch_state_walk(a, kda, cus, s);
+    if (walks > a.cus) return launch_state_walk(a, kda, a.cus, s);
     return kda ? dispatch_dims<bf16_t, true>(a, s) : dispatch_dims<bf16_t, false>(a, s);
   }
   return kda ? dispatch_dims<float, true>(a, s) : dispatch_dims<float, false>(a, s);

@@ -292,8 +292,8 @@ __global__ __launch_bounds__(64 * (TPW + 1), 1) void state_walk_kernel(PrefillAr
 // stages the chunks' NM blocks (shared by every tile) as above.  Workgroups of
 // TPW tiles: d_k / (16 TPW) of them for A, then d_v / (16 TPW) for B_seg, all
 // on one XCD.  Only segments that another segment of the same sequence
-// follows get a map; the first segment's A only when there is an initial
-// state.  A is stored in NM's fragment order (bf16) through an LDS transpose,
+// follows get a map, and the first segment has no A: its B_seg walk starts
+// from the initial state (copied to s0c on the way, prefill.h).  A is stored in NM's fragment order (bf16) through an LDS transpose,
 // B_seg in fp32 in the state kernel's tile order (prefill.h).
 template <typename T, int DK, int DV, bool KDA, bool SINGLE, int TPW>
 __global__ __launch_bounds__(64 * (TPW + 1), 1) void seg_map_kernel(PrefillArgs a) {
@@ -313,7 +313,7 @@ __global__ __launch_bounds__(64 * (TPW + 1), 1) void seg_map_kernel(PrefillArgs 
   if (sg.x < 0) return;
   if (sg.w == seq_seg_at<SINGLE>(a, sg.x).y - 1) return;  // the last segment's map is never applied
   const bool apart = part < NA;
-  if (apart && sg.w == 0 && !a.s0) return;  // the first segment's A acts on the initial state only
+  if (apart && sg.w == 0) return;  // the first segment's B walk starts from s0 instead
   const int nch = sg.z;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   auto blk = [&](int c) { return (size_t)(sg.y + min(c, nch - 1)) * a.Hv + h; };
@@ -353,10 +353,22 @@ __global__ __launch_bounds__(64 * (TPW + 1), 1) void seg_map_kernel(PrefillArgs 
   const int t = (apart ? part : part - NA) * TPW + wave;
   const int col = lane & 15, grp = lane >> 4;
   f32x4 H[RT];
+  // the first segment's B walk starts from the initial state, copied to s0c
+  const bool from_s0 = !apart && sg.w == 0 && a.s0;
+  const size_t sbase = ((size_t)sg.x * a.Hv + h) * DK * DV;
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) H[rt][e] = (apart && 16 * rt + 4 * grp + e == 16 * t + col) ? 1.f : 0.f;
+    for (int e = 0; e < 4; ++e) {
+      const int row = 16 * rt + 4 * grp + e;
+      if (from_s0) {  // uniform for the workgroup
+        const size_t i = sbase + (size_t)row * DV + dv_of(t, col);
+        H[rt][e] = a.s0[i];
+        a.s0c[i] = H[rt][e];
+      } else {
+        H[rt][e] = (apart && row == 16 * t + col) ? 1.f : 0.f;
+      }
+    }
 
   if (nch > 0) {
     const T *__restrict__ Bg = static_cast<const T *>(a.Bc);
@@ -491,7 +503,7 @@ __global__ __launch_bounds__(64 * (D / 16), 1) void seg_pair_kernel(PrefillArgs 
   const int4 sg = seg_info_at<SINGLE>(a, sgi);  // {sequence, first chunk, chunks, index in sequence}
   if (sg.x < 0) return;
   if (sg.w == seq_seg_at<SINGLE>(a, sg.x).y - 1) return;  // the last segment's map is never applied
-  const bool do_a = sg.w > 0 || a.s0;  // the first segment's A acts on the initial state only
+  const bool do_a = sg.w > 0;  // the first segment's B walk starts from s0 instead
   const int nch = sg.z;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int col = lane & 15, grp = lane >> 4;
@@ -511,12 +523,22 @@ __global__ __launch_bounds__(64 * (D / 16), 1) void seg_pair_kernel(PrefillArgs 
   };
 
   f32x4 HA[RT], HB[RT];  // tile w of A (columns 16w + col) and of B_seg (columns dv_of(w, col))
+  // the first segment's B walk starts from the initial state, copied to s0c
+  const bool from_s0 = sg.w == 0 && a.s0;
+  const size_t sbase = ((size_t)sg.x * a.Hv + h) * D * D;
 #pragma unroll
   for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      HA[rt][e] = (16 * rt + 4 * grp + e == 16 * w + col) ? 1.f : 0.f;
-      HB[rt][e] = 0.f;
+      const int row = 16 * rt + 4 * grp + e;
+      HA[rt][e] = (row == 16 * w + col) ? 1.f : 0.f;
+      if (from_s0) {  // uniform for the workgroup
+        const size_t i = sbase + (size_t)row * D + dv_of(w, col);
+        HB[rt][e] = a.s0[i];
+        a.s0c[i] = HB[rt][e];
+      } else {
+        HB[rt][e] = 0.f;
+      }
     }
 
   if (nch > 0) {

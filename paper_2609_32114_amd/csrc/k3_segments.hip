@@ -18,10 +18,11 @@
 //                 (fp32; the bf16 maps run on the staged walk, seg_map_kernel
 //                 in k2_walk.hip);
 //   seg_state     one workgroup per (segment, value head): applies the maps of
-//                 the earlier segments of its sequence to the initial state (a
-//                 short chain of d_k x d_k products), then walks its own
-//                 chunks, updating the state and emitting o; the last segment
-//                 of a sequence writes the final state.
+//                 the earlier segments of its sequence (a short chain of
+//                 d_k x d_k products; the first segment's B_seg already
+//                 carries the initial state), then walks its own chunks,
+//                 updating the state and emitting o; the last segment of a
+//                 sequence writes the final state.
 // The serial depth drops from the number of chunks n to about
 // seg_chunks (transfer) + n / seg_chunks (prefix) + seg_chunks (walk).
 //
@@ -429,13 +430,25 @@ __device__ __forceinline__ void transfer_part(const PrefillArgs &a, int s, int h
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
   HeadState<T, DK, NCOL> hs;
+  // the first segment's B walk starts from the initial state (copied to s0c
+  // for the first segment's state walk)
+  const bool from_s0 = !APART && sg.w == 0 && a.s0;
+  const size_t sbase = ((size_t)sg.x * a.Hv + h) * DK * DV;
 #pragma unroll
   for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        hs.H[ct][rt][e] = (APART && 16 * rt + 4 * grp + e == (w * CT + ct) * 16 + col) ? 1.f : 0.f;
+      for (int e = 0; e < 4; ++e) {
+        const int row = 16 * rt + 4 * grp + e;
+        if (from_s0) {  // uniform for the workgroup
+          const size_t i = sbase + (size_t)row * DV + dv_of(w * CT + ct, col);
+          hs.H[ct][rt][e] = a.s0[i];
+          a.s0c[i] = hs.H[ct][rt][e];
+        } else {
+          hs.H[ct][rt][e] = (APART && row == (w * CT + ct) * 16 + col) ? 1.f : 0.f;
+        }
+      }
   const int nch = sg.z;
   auto blk = [&](int c) { return (size_t)(sg.y + min(c, nch - 1)) * a.Hv + h; };
   auto no_out = [](int, const f32x4 (&)[CT][4]) {};
@@ -492,8 +505,8 @@ __global__ __launch_bounds__(kHeadThreads) void seg_transfer_kernel(PrefillArgs 
   if (sg.x < 0) return;
   if (sg.w == seq_seg_at<SINGLE>(a, sg.x).y - 1) return;  // the last segment's map is never applied
   if (part == 0) {
-    // the first segment's map acts on the initial state; with none only B_seg is used
-    if (sg.w == 0 && !a.s0) return;
+    // the first segment needs no A: its B walk starts from the initial state
+    if (sg.w == 0) return;
     transfer_part<T, DK, DV, KDA, true>(a, s, h, sg, lds);
   } else {
     transfer_part<T, DK, DV, KDA, false>(a, s, h, sg, lds);
@@ -562,24 +575,26 @@ __global__ __launch_bounds__(kHeadThreads) void seg_state_kernel(PrefillArgs a) 
   auto sidx = [&](int ct, int rt, int e) {
     return sbase + (size_t)(16 * rt + 4 * grp + e) * DV + dv_of(w * CT + ct, col);
   };
-  int j0 = ss.x;  // first segment map still to apply
-  if (sg.w > 0 && !a.s0) {
-    // a zero initial state: the first map reduces to its B_seg
-    const float *bm = a.Bseg + ((size_t)j0 * a.Hv + h) * ((size_t)DK * DV);
+  if (sg.w > 0) {
+    // the first segment's B_seg is the state entering the second segment (its
+    // walk started from s0); the maps of segments 1 .. sg.w - 1 follow
+    const float *bm = a.Bseg + ((size_t)ss.x * a.Hv + h) * ((size_t)DK * DV);
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) hs.H[ct][rt] = load4(bm + ((size_t)((w * CT + ct) * RT + rt) * 64 + lane) * 4);
-    ++j0;
+    if (ss.x + 1 < s) apply_maps(hs, a, ss.x + 1, s, h, lds);
   } else {
+    // s0 itself only when this workgroup is the sequence's only writer of
+    // s_final; otherwise the copy the segment maps made (s_final may alias s0)
+    const float *src = a.s0 ? (ss.y > 1 ? a.s0c : a.s0) : nullptr;
 #pragma unroll
     for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) hs.H[ct][rt][e] = a.s0 ? a.s0[sidx(ct, rt, e)] : 0.f;
+        for (int e = 0; e < 4; ++e) hs.H[ct][rt][e] = src ? src[sidx(ct, rt, e)] : 0.f;
   }
-  if (sg.w > 0 && j0 < s) apply_maps(hs, a, j0, s, h, lds);
 
   if (nch > 0) {
     const int tok0 = sg.w * a.seg_chunks * kChunk;  // first token of the segment inside its sequence

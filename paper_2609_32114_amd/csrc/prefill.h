@@ -51,6 +51,11 @@ constexpr int kPreAll = 7;
 //   Aseg  A_s in NM's fragment order and element type
 //   Bseg  B_s fp32, in Bc's accumulator-block order
 // Only segments followed by another segment of the same sequence have one.
+// The first segment of a sequence has no A: its B walk starts from the
+// initial state, so its B_s is the state entering the second segment, and
+// no later segment reads s0.  That walk also copies s0 to s0c, where the first
+// segment's state walk reads it: s_final may alias s0, and the last segment
+// writes s_final in the same launch in which the first one starts.
 struct PrefillArgs {
   const void *q, *k, *v;
   const float *g, *beta, *s0;
@@ -73,9 +78,11 @@ struct PrefillArgs {
   int4 *seg_info;      // [max_segs] {sequence (-1 = unused), first chunk, chunks, index in sequence}
   void *Aseg;
   float *Bseg;
+  float *s0c;          // [N, Hv, Dk, Dv] copy of s0 for sequences of several segments
   // 1: a single sequence, and no chunk index kernel ran: the kernels derive
   // the tables below from T and cu_seqlens (seq_info_at and friends)
   int single;
+  int cus;             // compute units of the device the call runs on
 };
 
 // The tables of the chunk index kernel, or for a single sequence (SINGLE:
@@ -150,7 +157,7 @@ hipError_t launch_chunk_local(const PrefillArgs &a, bool bf16, bool kda, hipStre
 // ops #5 + #6 over whole chains (every sequence one segment)
 hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
 // the bf16 whole-chain walk for batches with more walks than the device's
-// `cus` compute units (k2_walk.hip)
+// compute units (a.cus; k2_walk.hip)
 hipError_t launch_state_walk(const PrefillArgs &a, bool kda, int cus, hipStream_t stream);
 // the bf16 segment maps on the staged walk (k2_walk.hip)
 hipError_t launch_seg_maps(const PrefillArgs &a, bool kda, hipStream_t stream);
@@ -159,5 +166,10 @@ hipError_t launch_seg_transfer(const PrefillArgs &a, bool bf16, bool kda, hipStr
 hipError_t launch_seg_state(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
 // one decode step (N x Hv x Dv/64 workgroups)
 hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool kda, hipStream_t stream);
+// measured ceilings (k5_peaks.hip): a streaming copy of `bytes` (a multiple of
+// 16) on 8 workgroups per CU, and `blocks` workgroups of four waves running
+// `iters` rounds of 8 independent bf16 MFMAs each
+hipError_t launch_copy(const void *src, void *dst, size_t bytes, int cus, hipStream_t stream);
+hipError_t launch_mfma_loop(int blocks, int iters, float *sink, hipStream_t stream);
 
 }  // namespace hagdn

@@ -28,6 +28,10 @@ e^-52 per 64-token chunk, so inter-chunk propagation and s0 barely matter.
   "ks"   key stress: keys from a random 4-dim subspace per head, beta = 1
   "s0"   lm gates plus a nonzero 0.02*N(0,1) initial state
   "lg"   large gates: g = -softplus(3*N(0,1)) (exercises KDA exponent bounds)
+  "fg"   forget runs: base gates, except that runs of 8-24 consecutive tokens
+         (gaps of 8-56 tokens between them) have g = -30 (a gate of about
+         1e-13) on a random quarter of the key channels of each head (KDA),
+         or on the head's scalar gate (GDN)
 
 raw=True keeps the same draws as raw projections (q, k unnormalised, g and
 beta untransformed) for the kernels' in-kernel preprocessing.  Decode inputs
@@ -160,6 +164,21 @@ def make_case(kind="gdn", lengths=(256,), Hqk=1, Hv=1, Dk=64, Dv=64, dtype="f32"
         g = np.zeros(gshape, dtype=np.float32)
     elif variant == "lg":
         g = -_softplus(np.float32(3.0) * g_raw)
+    elif variant == "fg":
+        g = -_softplus(g_raw)
+        lanes = [(h, None) for h in range(Hv)] if kind == "gdn" else \
+            [(h, int(c)) for h in range(Hv) for c in rng.permutation(Dk)[:Dk // 4]]
+        for n in range(N):
+            for h, c in lanes:
+                t = int(cu[n]) + int(rng.integers(0, 32))
+                while t < cu[n + 1]:
+                    run = int(rng.integers(8, 24, endpoint=True))
+                    sl = slice(t, min(t + run, int(cu[n + 1])))
+                    if c is None:
+                        g[sl, h] = -30.0
+                    else:
+                        g[sl, h, c] = -30.0
+                    t += run + int(rng.integers(8, 56, endpoint=True))
     else:
         g = -_softplus(g_raw)
     beta = np.ones((T, Hv), dtype=np.float32) if variant == "ks" else _sigmoid(b_raw)

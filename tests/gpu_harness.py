@@ -13,6 +13,9 @@ from paper_2609_32114_amd.inputs import Inputs
 # and accumulation) 2e-2, on outputs and final states alike.
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
+# every comparison made in this process: (label, dtype, kind, max-rel o, max-rel s, nmse o, nmse s)
+RESULTS = []
+
 
 def oracle_threads():
     try:
@@ -87,7 +90,9 @@ def check_against_oracle(inp: Inputs, heads=None, tol=None, label=""):
     if heads is not None:
         o, sf = o[:, heads], sf[:, heads]
     eo, es = relerr(o, ro), relerr(sf, rs)
-    say(f"       max-rel o={eo:.3e} s={es:.3e}  nmse o={nmse(o, ro):.3e} s={nmse(sf, rs):.3e}")
+    no, ns = nmse(o, ro), nmse(sf, rs)
+    say(f"       max-rel o={eo:.3e} s={es:.3e}  nmse o={no:.3e} s={ns:.3e}")
+    RESULTS.append((label, inp.dtype, inp.kind, eo, es, no, ns))
     assert np.all(np.isfinite(o)) and np.all(np.isfinite(sf))
     assert eo <= tol, f"{label}: output max-rel {eo:.3e} > {tol}"
     assert es <= tol, f"{label}: state max-rel {es:.3e} > {tol}"

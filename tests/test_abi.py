@@ -98,41 +98,67 @@ def test_profile_requires_begin():
     assert lib.hagdn_profile_begin(0) == 1
 
 
+@needs_lib
+def test_segment_rule_depends_on_the_cu_count():
+    """The automatic segment length is a function of the device's compute
+    units: half the walks' share of the CUs moves the threshold, and L puts
+    about one segment workgroup on each CU."""
+    # 16 heads x 8 column tiles = 128 walk workgroups
+    assert P.segment_chunks_for(1, 7680, 16, 128, 256) == 12        # 120 chunks on 256 CUs: segments
+    assert P.segment_chunks_for(1, 7680, 16, 128, 128) == 120       # on 128 CUs the walks fill it
+    assert P.segment_chunks_for(1, 32768, 16, 128, 256) == 32       # 512 chunks: L = 512 x 16 / 256
+    assert P.segment_chunks_for(1, 32768, 16, 128, 128) == 64       # L = 512 x 16 / 128
+    assert P.segment_chunks_for(1, 32768, 16, 128, 80) == 103       # an 80-CU partition
+    assert P.segment_chunks_for(1, 32768, 16, 128, 64) == 512       # threshold 624 chunks: whole
+    assert P.segment_chunks_for(1, 8192, 16, 128, 256, kind="kda") == 8
+    assert P.segment_chunks_for(1, 8192, 16, 128, 128, kind="kda") == 128
+    with pytest.raises(P.HagdnError):
+        P.segment_chunks_for(1, 8192, 16, 128, 0)
+    # with no device to query (this host) the queries answer for 256 CUs
+    import torch
+    if not torch.cuda.is_available():
+        assert P.segment_chunks(1, 32768, 16, 128) == P.segment_chunks_for(1, 32768, 16, 128, 256)
+
+
 def test_segment_length_knob():
     import paper_2609_32114_amd as P
     P.load_library()
+
+    def seg_len(N, T, Hv, Dv, dtype=None, kind="gdn"):  # the rule on a 256-CU device
+        return P.segment_chunks_for(N, T, Hv, Dv, 256, dtype, kind)
+
     try:
-        # automatic: short chains stay one segment; long ones get about one
-        # segment workgroup per CU (n Hv / 256 chunks, at least 12)
-        assert P.segment_chunks(1, 256, 1, 64) == 4
-        assert P.segment_chunks(1, 0, 1, 64) == 1
-        assert P.segment_chunks(1, 4096, 16, 128) == 64
-        assert P.segment_chunks(1, 7616, 16, 128) == 119    # below 120 chunks: whole
-        assert P.segment_chunks(1, 7680, 16, 128) == 12     # 120 chunks
-        assert P.segment_chunks(1, 9216, 16, 128) == 12     # 144 chunks
-        assert P.segment_chunks(1, 12288, 16, 128) == 12
-        assert P.segment_chunks(1, 16384, 16, 128) == 16
-        assert P.segment_chunks(1, 32768, 16, 128) == 32
-        assert P.segment_chunks(1, 131072, 16, 128) == 128  # 2048 chunks
-        assert P.segment_chunks(1, 16384, 32, 128) == 256   # 256 walk workgroups: threshold 288
-        assert P.segment_chunks(1, 18368, 32, 128) == 287
-        assert P.segment_chunks(1, 18432, 32, 128) == 36    # 288 chunks: 288 x 32 / 256
-        assert P.segment_chunks(8, 34816, 32, 128) == 544   # short average chains: whole
+        # automatic (for a 256-CU device): short chains stay one segment; long
+        # ones get about one segment workgroup per CU (n Hv / 256 chunks, at least 12)
+        assert seg_len(1, 256, 1, 64) == 4
+        assert seg_len(1, 0, 1, 64) == 1
+        assert seg_len(1, 4096, 16, 128) == 64
+        assert seg_len(1, 7616, 16, 128) == 119    # below 120 chunks: whole
+        assert seg_len(1, 7680, 16, 128) == 12     # 120 chunks
+        assert seg_len(1, 9216, 16, 128) == 12     # 144 chunks
+        assert seg_len(1, 12288, 16, 128) == 12
+        assert seg_len(1, 16384, 16, 128) == 16
+        assert seg_len(1, 32768, 16, 128) == 32
+        assert seg_len(1, 131072, 16, 128) == 128  # 2048 chunks
+        assert seg_len(1, 16384, 32, 128) == 256   # 256 walk workgroups: threshold 288
+        assert seg_len(1, 18368, 32, 128) == 287
+        assert seg_len(1, 18432, 32, 128) == 36    # 288 chunks: 288 x 32 / 256
+        assert seg_len(8, 34816, 32, 128) == 544   # short average chains: whole
         # KDA segments from 112 chunks, L at least 8
-        assert P.segment_chunks(1, 5568, 16, 128, kind="kda") == 87
-        assert P.segment_chunks(1, 5632, 16, 128, kind="kda") == 8
-        assert P.segment_chunks(1, 8192, 16, 128, kind="kda") == 8
-        assert P.segment_chunks(1, 12288, 16, 128, kind="kda") == 12
-        assert P.segment_chunks(1, 8192, 16, 128, kind="gdn") == 12
-        assert P.segment_chunks(1, 6144, 16, 128, kind="gdn") == 96
+        assert seg_len(1, 5568, 16, 128, kind="kda") == 87
+        assert seg_len(1, 5632, 16, 128, kind="kda") == 8
+        assert seg_len(1, 8192, 16, 128, kind="kda") == 8
+        assert seg_len(1, 12288, 16, 128, kind="kda") == 12
+        assert seg_len(1, 8192, 16, 128, kind="gdn") == 12
+        assert seg_len(1, 6144, 16, 128, kind="gdn") == 96
         with pytest.raises(ValueError):
-            P.segment_chunks(1, 8192, 16, 128, kind="mamba")
+            seg_len(1, 8192, 16, 128, kind="mamba")
         P.set_segment_chunks(8)
-        auto = P.segment_chunks(1, 4096, 16, 128)
+        auto = seg_len(1, 4096, 16, 128)
         assert auto == 8
         ws_auto = P.workspace_size("gdn", 1, 4096, 16, 16, 128, 128, P.HAGDN_BF16)  # L = 8
         P.set_segment_chunks(2)
-        assert P.segment_chunks(1, 4096, 16, 128) == 2
+        assert seg_len(1, 4096, 16, 128) == 2
         ws_small = P.workspace_size("gdn", 1, 4096, 16, 16, 128, 128, P.HAGDN_BF16)
         assert ws_small > ws_auto  # more segment maps
         P.set_segment_chunks(64)   # one segment: no maps at all
@@ -143,17 +169,17 @@ def test_segment_length_knob():
         # the cap: 64 L Hv Dv elements stay below 2 GiB, forced or automatic
         import torch
         P.set_segment_chunks(1 << 20)
-        assert P.segment_chunks(1, 4096, 16, 128) == 8191                      # bf16: 2^31 / 256 KiB
-        assert P.segment_chunks(1, 4096, 16, 128, torch.float32) == 4095       # fp32: 2^31 / 512 KiB
-        assert P.segment_chunks(1, 32832, 128, 128, torch.float32) == 511
-        assert P.segment_chunks(1, 4096, 65535, 128, torch.float32) == 1       # 64 rows: 2147450880 B
+        assert seg_len(1, 4096, 16, 128) == 8191                      # bf16: 2^31 / 256 KiB
+        assert seg_len(1, 4096, 16, 128, torch.float32) == 4095       # fp32: 2^31 / 512 KiB
+        assert seg_len(1, 32832, 128, 128, torch.float32) == 511
+        assert seg_len(1, 4096, 65535, 128, torch.float32) == 1       # 64 rows: 2147450880 B
         P.set_segment_chunks(0)
-        L = P.segment_chunks(4096, 4096 * 2048, 16, 128)   # short chains, 8M tokens: whole, then capped
+        L = seg_len(4096, 4096 * 2048, 16, 128)   # short chains, 8M tokens: whole, then capped
         assert L == 8191 and 64 * L * 16 * 128 * 2 < 2 ** 31 <= 64 * (L + 1) * 16 * 128 * 2
-        assert P.segment_chunks(1, 32832, 128, 128, torch.float32) == 511    # whole (1024 walks), capped
+        assert seg_len(1, 32832, 128, 128, torch.float32) == 511    # whole (1024 walks), capped
     finally:
         P.set_segment_chunks(0)
-    assert P.segment_chunks(1, 4096, 16, 128) == 64
+    assert P.segment_chunks_for(1, 4096, 16, 128, 256) == 64
 
 
 def _call_ex(lib, kind="gdn", pre=0, **kw):
