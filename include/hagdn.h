@@ -242,6 +242,29 @@ int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv, int dtype, int kda)
  * logic only.  -1 on invalid arguments (cus < 1 included). */
 int hagdn_segment_chunks_for(int N, int T_total, int Hv, int Dv, int dtype, int kda, int cus);
 
+/* Allocation-free prefill, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): gdn_prefill_ex (kda = 0) or kda_prefill_ex (kda = 1) with the
+ * same arguments except the workspace, which is a static device array of
+ * hagdn_prefill_noalloc_capacity() bytes (128 MiB) that the library holds on
+ * each device it runs on until the process ends.  The caller still provides
+ * every input and output.  A call whose workspace (the *_workspace_size of
+ * its sizes) exceeds the capacity returns HAGDN_EWORKSPACE before anything is
+ * enqueued: 128 MiB covers, e.g., one 4096-token sequence at 16 value heads of
+ * d = 128 (bf16: 98 MiB; about 1,330 (chunk, value head) blocks at d = 128).
+ * Nothing is allocated or freed: no hipMalloc, hipFree or allocating library
+ * call.  All calls on one device share the one array, so calls that overlap
+ * in time on a device (other streams, other host threads) race and must be
+ * serialised by the caller; calls in one stream are ordered.  Nothing in the
+ * array needs to start at zero: every region is written before it is read.
+ * The device status word of hagdn_device_status is not readable for these
+ * calls.  Returns a hagdn_status. */
+int hagdn_prefill_noalloc(int kda, const void *q, const void *k, const void *v, const float *g,
+                          const float *beta, const float *s0, const int32_t *cu_seqlens, int N,
+                          int T_total, int Hqk, int Hv, int Dk, int Dv, float scale, int dtype,
+                          int pre, void *o, float *s_final, void *stream);
+size_t hagdn_prefill_noalloc_capacity(void);
+
 /* Measurement aids (no prefill or decode call uses them): the ceilings that
  * roofline fractions can be quoted against, measured on the current device.
  *   hagdn_measure_copy  enqueues one streaming copy of `bytes` (a multiple of

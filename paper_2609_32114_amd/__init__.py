@@ -69,6 +69,10 @@ _SYMBOLS = {
     "hagdn_segment_chunks": (ctypes.c_int, [ctypes.c_int] * 6),
     "hagdn_segment_chunks_for": (ctypes.c_int, [ctypes.c_int] * 7),
     "hagdn_workspace_region": (ctypes.c_int, [ctypes.c_int] * 9 + [ctypes.POINTER(ctypes.c_size_t)] * 2),
+    "hagdn_prefill_noalloc": (ctypes.c_int, [ctypes.c_int] + [ctypes.c_void_p] * 7 + [ctypes.c_int] * 6 +
+                              [ctypes.c_float, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                               ctypes.c_void_p, ctypes.c_void_p]),
+    "hagdn_prefill_noalloc_capacity": (ctypes.c_size_t, []),
     "hagdn_measure_copy": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "hagdn_measure_mfma": (ctypes.c_int, [ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t,
                                           ctypes.POINTER(ctypes.c_double), ctypes.c_void_p]),

@@ -353,9 +353,58 @@ int decode(bool kda, const void *q, const void *k, const void *v, const float *g
   return HAGDN_OK;
 }
 
+// ------------------------------------------------- allocation-free entry point
+// The workspace of hagdn_prefill_noalloc: a file-scope device array, one copy
+// per device, held until the process ends.  Host code must never pass the
+// array's name to a kernel or a copy (it names a host-side stand-in); it uses
+// the device address hipGetSymbolAddress returns, looked up once per device
+// with that device current.
+constexpr size_t kScratchBytes = (size_t)128 << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::atomic<void *> g_scratch_ptr[kMaxScratchDevices];
+
+// Device address of `scratch` on the current device (looked up on first use).
+hipError_t scratch_address(void **out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  void *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev].store(p, std::memory_order_release);  // the same address from any thread
+  }
+  *out = p;
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
+
+int hagdn_prefill_noalloc(int kda, const void *q, const void *k, const void *v, const float *g,
+                          const float *beta, const float *s0, const int32_t *cu_seqlens, int N,
+                          int T_total, int Hqk, int Hv, int Dk, int Dv, float scale, int dtype,
+                          int pre, void *o, float *s_final, void *stream) {
+  int rc = check_shapes(N, T_total, Hqk, Hv, Dk, Dv, dtype);
+  if (rc != HAGDN_OK) return rc;
+  Layout L;
+  if (!make_layout(N, T_total, Hv, Dk, Dv, dtype == HAGDN_BF16 ? 2 : 4, kda != 0, query_cus(), &L))
+    return HAGDN_EINVAL;
+  if (L.total > kScratchBytes)
+    return fail(HAGDN_EWORKSPACE, "the call needs %zu bytes of workspace; hagdn_prefill_noalloc holds %zu",
+                L.total, kScratchBytes);
+  void *ws = nullptr;
+  hipError_t e = scratch_address(&ws);
+  if (e != hipSuccess) return fail(HAGDN_EHIP, "static workspace: %s", hipGetErrorString(e));
+  return prefill(kda != 0, q, k, v, g, beta, s0, cu_seqlens, N, T_total, Hqk, Hv, Dk, Dv, scale, dtype,
+                 pre, o, s_final, ws, kScratchBytes, stream);
+}
+
+size_t hagdn_prefill_noalloc_capacity(void) { return kScratchBytes; }
 
 size_t gdn_prefill_workspace_size(int N, int T_total, int Hqk, int Hv, int Dk, int Dv, int dtype) {
   return workspace_size(false, N, T_total, Hqk, Hv, Dk, Dv, dtype);
