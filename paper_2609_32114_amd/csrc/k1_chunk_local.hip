@@ -687,23 +687,27 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
     for (int n = 0; n < VT; ++n) store4(sUt + swz<T, L::LDT>(16 * n + col, tpos), accU[n]);
   }
   // ---- Kt = (K * e^(gamma_last - gamma))^T in place of the staged keys, tokens
-  //      kmap-permuted like sWt / sUt (thread d < DK owns channel row d)
-  if (tid < DK) {
-    const int d = tid;
-    uint4 row[kChunk / V];
+  //      kmap-permuted like sWt / sUt (kmap moves tokens only inside their
+  //      32-token block).  Thread tid < 2 DK takes channel row tid % DK and
+  //      32-token block tid / DK, so at d_k = 128 all four waves share it.
+  if (tid < DK * (kChunk / 32)) {
+    constexpr int UH = 32 / V;  // 16-byte vectors per 32-token block
+    const int d = tid % DK, base = 32 * (tid / DK);
+    uint4 row[UH];
 #pragma unroll
-    for (int u = 0; u < kChunk / V; ++u) row[u] = *reinterpret_cast<const uint4 *>(sKt + swz<T, L::LDT>(d, u * V));
+    for (int u = 0; u < UH; ++u) row[u] = *reinterpret_cast<const uint4 *>(sKt + swz<T, L::LDT>(d, base + u * V));
 #pragma unroll
-    for (int u = 0; u < kChunk / V; ++u) {
+    for (int u = 0; u < UH; ++u) {
       float outv[V];
 #pragma unroll
       for (int j = 0; j < V; ++j) {
-        const int p = u * V + j;
-        const int s = (p & ~31) + kmap((p & 31) >> 3, p & 7);
-        const float ex = KDA ? __expf(sGam[gam_at<DK>(kChunk - 1, d)] - sGam[gam_at<DK>(s, d)]) : sKdec[s];
+        const int p = u * V + j;            // position inside the 32-token block
+        const int s = kmap(p >> 3, p & 7);  // token held there, relative to base
+        const float ex = KDA ? __expf(sGam[gam_at<DK>(kChunk - 1, d)] - sGam[gam_at<DK>(base + s, d)])
+                             : sKdec[base + s];
         outv[j] = V16::get(row[s / V], s % V) * ex;
       }
-      *reinterpret_cast<uint4 *>(sKt + swz<T, L::LDT>(d, u * V)) = V16::pack(outv);
+      *reinterpret_cast<uint4 *>(sKt + swz<T, L::LDT>(d, base + u * V)) = V16::pack(outv);
     }
   }
   {  // chunk decay e^gamma_last
