@@ -63,10 +63,12 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 def kernel_source_hash(name: str) -> str:
     """Hash of the sources a kernel is built from (traffic counters go stale when they change)."""
     csrc = os.path.join(ROOT, "paper_2609_32114_amd", "csrc")
-    files = {"chunk_local": ("k1_chunk_local.hip",),
-             "state_prop": ("k2_state_prop.hip", "k2_walk.hip", "k3_segments.hip"),
+    files = {"chunk_local": ("k1_chunk_local.hip", "state_walk.h"),
+             "state_prop": ("k2_state_prop.hip", "state_walk.h", "k2_walk.hip", "k3_segments.hip"),
              "seg_transfer": ("k3_segments.hip", "k2_walk.hip"), "chunk_index": ("k0_chunk_index.hip",),
-             "decode": ("k4_decode.hip",)}
+             "decode": ("k4_decode.hip",),
+             "overlap_setup": ("k1_chunk_local.hip",),
+             "overlapped": ("k1_chunk_local.hip", "state_walk.h")}
     h = hashlib.sha256()
     for f in files[name] + ("device.h", "prefill.h"):
         with open(os.path.join(csrc, f), "rb") as fh:

@@ -83,8 +83,17 @@ typedef enum {
 typedef enum { HAGDN_F32 = 0, HAGDN_BF16 = 1 } hagdn_dtype;
 
 /* Device-side status word written by every prefill call (by its first
- * kernel, or for a single sequence by its state kernel). */
-typedef enum { HAGDN_DEV_OK = 0, HAGDN_DEV_BAD_SEQLENS = 1 } hagdn_device_code;
+ * kernel, or for a single sequence by its state kernel or, in an overlapped
+ * call, by the setup kernel).  HAGDN_DEV_WAIT_TIMEOUT: in an overlapped call
+ * (hagdn_set_overlap) a walk stopped waiting, after about 0.4 s, for a chunk
+ * that its XCD's chunk-local work never published; the outputs are invalid.
+ * Not expected: it would take a dispatch that leaves some XCD without the
+ * workgroups of its queue (see hagdn_set_overlap). */
+typedef enum {
+  HAGDN_DEV_OK = 0,
+  HAGDN_DEV_BAD_SEQLENS = 1,
+  HAGDN_DEV_WAIT_TIMEOUT = 2
+} hagdn_device_code;
 
 /* Bytes of device workspace gdn_prefill needs for these sizes (0 if the
  * arguments are invalid; hagdn_last_error() then says why).  The workspace
@@ -96,7 +105,9 @@ typedef enum { HAGDN_DEV_OK = 0, HAGDN_DEV_BAD_SEQLENS = 1 } hagdn_device_code;
  * Chunk-Seg-Seg mapping; see hagdn_segment_chunks) it also holds one segment
  * map, Dk*Dk elements plus Dk*Dv floats, per (segment, value head) for
  * segments bounded by (T/64 + N) / L + N, and a copy of s0 (Dk*Dv floats
- * per sequence and value head).  The size depends on the segment length L in
+ * per sequence and value head).  It always holds 2 KiB plus 4 bytes per
+ * (chunk, value head) for the queues and ready flags of the overlapped
+ * launch (hagdn_set_overlap).  The size depends on the segment length L in
  * force (hagdn_set_segment_chunks) and on the current device's compute units
  * (see hagdn_segment_chunks): query it after setting, with the device the
  * call will run on current. */
@@ -241,6 +252,31 @@ int hagdn_segment_chunks(int N, int T_total, int Hv, int Dv, int dtype, int kda)
 /* The same rule for a device of `cus` compute units (no device query): host
  * logic only.  -1 on invalid arguments (cus < 1 included). */
 int hagdn_segment_chunks_for(int N, int T_total, int Hv, int Dv, int dtype, int kda, int cus);
+
+/* Overlapped launch.  The state walk of chunk c needs only chunks 0..c's
+ * chunk-local factors, so a call whose chains are walked whole (no segment
+ * maps: see hagdn_segment_chunks) runs the chunk-local work (operators #1-#4
+ * and the state-independent factors of #5-#6) and the walks (#5 fused with #6)
+ * in ONE launch: walk workgroups wait, chunk by chunk, for ready flags that the
+ * chunk-local workgroups set once a block's factors are stored, instead of
+ * for the whole chunk-local kernel (Sec. 4's cross-operator fusion, with the
+ * Map of later chunks running beside the Reduce of earlier ones).  Each
+ * workgroup reads the id of the XCD it runs on and takes its work from that
+ * XCD's queues: value heads h = x (mod 8) are produced and walked on XCD x,
+ * so the factors and flags pass through one L2 (the L2s of different XCDs are
+ * not coherent within a kernel).  It applies to bf16 calls with Dk = Dv = 128,
+ * on devices of at least 256 CUs (8 XCDs), whose walks (N x Hv x Dv/16
+ * workgroups) fit in half the CUs; other calls run the kernels one after
+ * another.  Results are bit-identical either way.  A tiny setup kernel clears
+ * the queues and flags first (in the workspace).  hagdn_set_overlap(0) turns
+ * it off for every later call in the process, (1) back on (the default).
+ * Returns HAGDN_OK or HAGDN_EINVAL. */
+int hagdn_set_overlap(int on);
+
+/* 1 if a call with these sizes (kda: 0 gdn, 1 kda) would take the overlapped
+ * launch on a device of `cus` compute units with the switch as it is now, 0
+ * if not, -1 on invalid arguments.  Host logic only. */
+int hagdn_overlap_for(int N, int T_total, int Hv, int Dk, int Dv, int dtype, int kda, int cus);
 
 /* Allocation-free prefill, for callers that cannot allocate device memory
  * (code under HIP graph capture, tight serving loops, harnesses that forbid

@@ -28,6 +28,7 @@ import os
 
 __all__ = ["gdn_prefill", "kda_prefill", "gdn_decode", "kda_decode", "workspace_size",
            "device_status", "library_path", "load_library", "profile_begin", "profile_end", "kernel_names", "set_segment_chunks",
+           "set_overlap", "overlap_for",
            "segment_chunks", "segment_chunks_for", "workspace_region", "measure_copy", "measure_mfma",
            "HagdnError"]
 
@@ -36,7 +37,7 @@ _LIB_PATH = os.path.join(_HERE, "libhagdn.so")
 _lib = None
 
 HAGDN_F32, HAGDN_BF16 = 0, 1
-DEV_OK, DEV_BAD_SEQLENS = 0, 1
+DEV_OK, DEV_BAD_SEQLENS, DEV_WAIT_TIMEOUT = 0, 1, 2
 # preprocessing flags (hagdn_pre_flags)
 PRE_QK_L2NORM, PRE_GATE_SOFTPLUS, PRE_BETA_SIGMOID = 1, 2, 4
 PRE_ALL = 7
@@ -66,6 +67,8 @@ _SYMBOLS = {
     "hagdn_kernel_name": (ctypes.c_char_p, [ctypes.c_int]),
     "hagdn_version": (ctypes.c_int, []),
     "hagdn_set_segment_chunks": (ctypes.c_int, [ctypes.c_int]),
+    "hagdn_set_overlap": (ctypes.c_int, [ctypes.c_int]),
+    "hagdn_overlap_for": (ctypes.c_int, [ctypes.c_int] * 8),
     "hagdn_segment_chunks": (ctypes.c_int, [ctypes.c_int] * 6),
     "hagdn_segment_chunks_for": (ctypes.c_int, [ctypes.c_int] * 7),
     "hagdn_workspace_region": (ctypes.c_int, [ctypes.c_int] * 9 + [ctypes.POINTER(ctypes.c_size_t)] * 2),
@@ -300,6 +303,27 @@ def set_segment_chunks(chunks: int):
     rc = lib.hagdn_set_segment_chunks(int(chunks))
     if rc != 0:
         raise HagdnError(rc, _err(lib))
+
+
+def set_overlap(on: bool):
+    """Whether later calls that qualify run the chunk-local work and the state
+    walks in one overlapped launch (True, the default) or one after another."""
+    lib = load_library()
+    rc = lib.hagdn_set_overlap(1 if on else 0)
+    if rc != 0:
+        raise HagdnError(rc, _err(lib))
+
+
+def overlap_for(N: int, T: int, Hv: int, Dk: int, Dv: int, dtype_code: int, kind: str = "gdn",
+                cus: int = 256) -> bool:
+    """Whether a call with these sizes takes the overlapped launch on a device
+    of `cus` compute units (host logic only)."""
+    lib = load_library()
+    r = lib.hagdn_overlap_for(int(N), int(T), int(Hv), int(Dk), int(Dv), int(dtype_code),
+                              int(kind == "kda"), int(cus))
+    if r < 0:
+        raise HagdnError(1, _err(lib))
+    return bool(r)
 
 
 def segment_chunks(N: int, T: int, Hv: int, Dv: int, dtype=None, kind: str = "gdn") -> int:

@@ -52,6 +52,10 @@ def kernel_bytes(kernel: str, T_total: int, N: int, Hqk: int, Hv: int, dk: int, 
                     the segment maps A (dk x dk) and B_seg (dk x dv fp32) out
       state_prop    -M, B, decay, Q', O_loc, the segment maps and s0 in; o, s_final
                     out (operators #5 and #6)
+      overlap_setup the overlapped launch's queues (2 KiB) and ready flags cleared
+      overlapped    chunk_local and state_prop in one launch: q, k, v, gate, beta
+                    and s0 in, o and s_final out; the factors pass between its
+                    workgroups (through the L2 of their XCD) and are not counted
     """
     e = elt_bytes
     chunks = (T_total + chunk - 1) // chunk
@@ -76,6 +80,11 @@ def kernel_bytes(kernel: str, T_total: int, N: int, Hqk: int, Hv: int, dk: int, 
         rd += state if with_s0 else 0
         wr = T_total * Hv * dv * e + state
         return rd + wr
+    if kernel == "overlap_setup":
+        return 2048 + cb * 4
+    if kernel == "overlapped":
+        rd = T_total * (2 * Hqk * dk * e + Hv * dv * e + gate + Hv * 4) + (state if with_s0 else 0)
+        return rd + T_total * Hv * dv * e + state
     raise KeyError(kernel)
 
 

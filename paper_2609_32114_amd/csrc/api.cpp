@@ -45,13 +45,16 @@ int fail(int code, const char *fmt, ...) {
 }
 
 constexpr size_t kAlign = 256;
-constexpr int kNumKernels = 5;
+constexpr int kNumKernels = 7;
 const char *const kKernelNames[kNumKernels] = {"chunk_index", "chunk_local", "seg_transfer", "state_prop",
-                                               "decode"};
+                                               "decode",      "overlap_setup", "overlapped"};
 constexpr int kDecodeKernel = 4;
 
 // Chunks per segment of the state chain; 0 = chosen per call (seg_chunks).
 std::atomic<int> g_seg_override{0};
+// 1: calls that can run the chunk-local work and the state walks in one
+// overlapped launch do so (hagdn_set_overlap).
+std::atomic<int> g_overlap{1};
 constexpr int kMaxSegChunks = 1 << 20;
 // Compute units assumed by the size and segment-length queries when no HIP
 // device can be queried (a host without a GPU: nothing can launch there, the
@@ -134,7 +137,7 @@ bool add_ok(size_t a, size_t b, size_t *out) { return !__builtin_add_overflow(a,
 
 // Byte offsets of every workspace region (each 256-byte aligned).
 struct Layout {
-  size_t status, seq_info, chunk_info, NM, Bc, Qp, Ol, dec, seq_seg, seg_info, Aseg, Bseg, s0c, total;
+  size_t status, seq_info, chunk_info, NM, Bc, Qp, Ol, dec, seq_seg, seg_info, Aseg, Bseg, s0c, ovl, total;
   int max_chunks, seg_chunks, max_segs;
 };
 
@@ -179,6 +182,8 @@ bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, bool kda, int
   L->Aseg = region((size_t)Dk * Dk, esz, maps ? sblocks : 0);
   L->Bseg = region((size_t)Dk * Dv, sizeof(float), maps ? sblocks : 0);
   L->s0c = region((size_t)Dk * Dv, sizeof(float), maps ? (size_t)N * (size_t)Hv : 0);
+  // overlapped launch: per-XCD queues, then a ready flag per block
+  L->ovl = region(1, sizeof(int), (size_t)hagdn::kOvlFlags + blocks);
   L->total = (off + kAlign - 1) / kAlign * kAlign;
   if (!ok) fail(HAGDN_EINVAL, "workspace size overflows");
   return ok;
@@ -195,6 +200,18 @@ int check_shapes(int N, int T, int Hqk, int Hv, int Dk, int Dv, int dtype) {
   if (dtype != HAGDN_F32 && dtype != HAGDN_BF16)
     return fail(HAGDN_EUNSUPPORTED, "dtype %d unsupported", dtype);
   return HAGDN_OK;
+}
+
+// Whether a call runs the chunk-local kernel and the whole-chain walks in one
+// overlapped launch (k1_chunk_local.hip, launch_overlapped): chains walked
+// whole by the four-wave walk, an instance for the operands, a device of at
+// least 8 XCDs x 32 CUs (XCC ids 0-7) and walks on at most half the CUs, so
+// that the chunk-local work keeps most of the device.
+bool overlap_applies(bool bf16, int Dk, int Dv, bool maps, int N, int Hv, int cus) {
+  if (!g_overlap.load(std::memory_order_relaxed) || maps || !hagdn::overlap_supported(bf16, Dk, Dv)) return false;
+  if (cus < hagdn::kXcdCount * 32) return false;
+  const long walks = (long)N * Hv * (Dv / 16);
+  return walks <= cus / 2;
 }
 
 size_t workspace_size(bool kda, int N, int T, int Hqk, int Hv, int Dk, int Dv, int dtype) {
@@ -276,7 +293,10 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   a.s0c = reinterpret_cast<float *>(w + L.s0c);
   a.single = N == 1 ? 1 : 0;  // the kernels derive a single sequence's tables themselves
   a.cus = cus;
+  a.ovl = reinterpret_cast<int *>(w + L.ovl);
+  a.ovl_walk_wgs = 0;
   const bool maps = (T + hagdn::kChunk - 1) / hagdn::kChunk > L.seg_chunks;
+  const bool overlap = T > 0 && overlap_applies(bf16, Dk, Dv, maps, N, Hv, cus);
 
   hipStream_t st = static_cast<hipStream_t>(stream_);
   hipEvent_t *ev = nullptr;
@@ -299,6 +319,15 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   if (!a.single) {
     if ((e = hagdn::launch_chunk_index(a, st)) != hipSuccess) goto hip_fail;
     if ((e = mark(1)) != hipSuccess) goto hip_fail;
+  }
+  if (overlap) {
+    // flags and queues cleared (and a single sequence's status word written),
+    // then the chunk-local items and the walks in one launch
+    if ((e = hagdn::launch_overlap_setup(a, st)) != hipSuccess) goto hip_fail;
+    if ((e = mark(6)) != hipSuccess) goto hip_fail;
+    if ((e = hagdn::launch_overlapped(a, kda, st)) != hipSuccess) goto hip_fail;
+    if ((e = mark(7)) != hipSuccess) goto hip_fail;
+    return HAGDN_OK;
   }
   if ((e = hagdn::launch_chunk_local(a, bf16, kda, st)) != hipSuccess) goto hip_fail;
   if ((e = mark(2)) != hipSuccess) goto hip_fail;
@@ -530,6 +559,21 @@ int hagdn_kernel_count(void) { return kNumKernels; }
 const char *hagdn_kernel_name(int i) { return (i >= 0 && i < kNumKernels) ? kKernelNames[i] : ""; }
 
 int hagdn_version(void) { return 100; }
+
+int hagdn_set_overlap(int on) {
+  if (on != 0 && on != 1) return fail(HAGDN_EINVAL, "overlap switch must be 0 or 1 (got %d)", on);
+  g_overlap.store(on, std::memory_order_relaxed);
+  return HAGDN_OK;
+}
+
+int hagdn_overlap_for(int N, int T_total, int Hv, int Dk, int Dv, int dtype, int kda, int cus) {
+  if (check_shapes(N, T_total, 1, Hv, Dk, Dv, dtype) != HAGDN_OK) return -1;
+  if (cus < 1) return fail(HAGDN_EINVAL, "cus must be >= 1 (got %d)", cus), -1;
+  const size_t esz = dtype == HAGDN_BF16 ? 2 : 4;
+  const int L = seg_chunks(N, T_total, Hv, Dv, esz, kda != 0, cus);
+  const bool maps = (T_total + hagdn::kChunk - 1) / hagdn::kChunk > L;
+  return T_total > 0 && overlap_applies(dtype == HAGDN_BF16, Dk, Dv, maps, N, Hv, cus) ? 1 : 0;
+}
 
 int hagdn_set_segment_chunks(int chunks) {
   if (chunks < 0 || chunks > kMaxSegChunks)

@@ -38,10 +38,12 @@
 // solves T by forward substitution (lane j owns column j) while waves 1-3
 // write the decay; wave i computes token block i of W and U~ into LDS; then
 // the four reduce-side products are split over the waves.
+#include <algorithm>
 #include <atomic>
 
 #include "device.h"
 #include "prefill.h"
+#include "state_walk.h"
 
 namespace hagdn {
 
@@ -150,6 +152,48 @@ __device__ __forceinline__ LocalItem local_item(const PrefillArgs &a, int b) {
     }
   }
   return it;
+}
+
+// Overlapped launch: the next item of this XCD's queue.  XCD x serves the
+// value heads h = x (mod 8) (ovl_heads), chunk-major, so the blocks of a head
+// are produced in chunk order on the XCD whose L2 that head's walks read.
+__device__ __forceinline__ LocalItem ovl_item(const PrefillArgs &a) {
+  __shared__ int ticket;
+  const int x = xcc_id();
+  if (threadIdx.x == 0) ticket = atomicAdd(a.ovl + kOvlLocalQ + kOvlStride * x, 1);
+  __syncthreads();
+  const int t = ticket;
+  const int hx = ovl_heads(a.Hv, x);
+  LocalItem it{0, 0, 0, 0};
+  if (hx > 0 && t < a.max_chunks * hx) {
+    it.c = t / hx;
+    it.h = x + kXcdCount * (t % hx);
+    if (a.single) {
+      it.start = it.c * kChunk;
+      it.len = max(0, min(kChunk, a.T - it.start));
+    } else {
+      const int4 ci = a.chunk_info[it.c];
+      it.start = ci.y;
+      it.len = ci.z;
+    }
+  }
+  return it;
+}
+
+// Overlapped launch, walk role: the next whole-chain walk tile of this XCD's
+// queue (value heads h = x (mod 8), every sequence, every d_v tile).
+template <typename T, int DK, int DV, bool KDA, bool SINGLE>
+__device__ __forceinline__ void ovl_walk(const PrefillArgs &a) {
+  constexpr int NT = DV / 16;
+  __shared__ int ticket;
+  const int x = xcc_id();
+  if (threadIdx.x == 0) ticket = atomicAdd(a.ovl + kOvlWalkQ + kOvlStride * x, 1);
+  __syncthreads();
+  const int t = ticket;
+  const int hx = ovl_heads(a.Hv, x);
+  if (hx == 0 || t >= a.N * hx * NT) return;  // uniform for the workgroup
+  const int j = t / NT, n = j / hx, h = x + kXcdCount * (j % hx);
+  walk_tile<T, DK, DV, KDA, SINGLE, true>(a, n * a.Hv + h, t % NT);
 }
 
 // Global inputs of one item (padded tokens: zeros).
@@ -274,9 +318,12 @@ struct LocalIn {
 };
 
 // PRE: the call carries preprocessing flags (a separate instance, so that the
-// plain path keeps its register budget).
-template <typename T, int DK, int DV, bool KDA, bool PRE>
-__global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void chunk_local_kernel(PrefillArgs a) {
+// plain path keeps its register budget).  OVL: the overlapped launch (1: a
+// single sequence, 2: a batch): workgroups below a.ovl_walk_wgs walk whole
+// chains (ovl_walk), the others take chunk-local items from their XCD's
+// queue and publish each block's ready flag once its factors are stored.
+template <typename T, int DK, int DV, bool KDA, bool PRE, int OVL = 0>
+__global__ __launch_bounds__(kLocalThreads, OVL || (KDA && sizeof(T) == 2) ? 2 : 1) void chunk_local_kernel(PrefillArgs a) {
   using L = LocalLayout<T, DK, DV, KDA>;
   using E = Elt<T>;
   using V16 = Vec16<T>;
@@ -286,7 +333,13 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
   constexpr int KPW = KT / 4;             // d_k tiles per wave in the reduce-side products
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
-  const LocalItem cur = local_item(a, blockIdx.x);
+  if constexpr (OVL != 0) {
+    if ((int)blockIdx.x < a.ovl_walk_wgs) {
+      ovl_walk<T, DK, DV, KDA, OVL == 1>(a);
+      return;
+    }
+  }
+  const LocalItem cur = OVL ? ovl_item(a) : local_item(a, blockIdx.x);
   if (cur.len <= 0) return;  // past the last chunk: uniform for the workgroup
   In in;
   in.load_kvg(a, cur);
@@ -818,11 +871,19 @@ __global__ __launch_bounds__(kLocalThreads, KDA && sizeof(T) == 2 ? 2 : 1) void 
       store4(ol_out + ((size_t)m * 64 + lane) * 16 + 4 * wave, acc);
     }
   }
+  if constexpr (OVL != 0) {
+    // Every wave's factor stores have completed, so they sit in this XCD's
+    // L2, before the block's ready flag is set there (an atomic: it executes
+    // in the L2, where the walks' atomic reads of the flag see it).
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (tid == 0) __hip_atomic_fetch_or(a.ovl + kOvlFlags + blk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 // The kernel's dynamic LDS exceeds the default 64 KiB limit for some
 // instances: raise it once per device.
-template <typename T, int DK, int DV, bool KDA, bool PRE>
+template <typename T, int DK, int DV, bool KDA, bool PRE, int OVL = 0>
 static hipError_t set_lds_limit() {
   using L = LocalLayout<T, DK, DV, KDA>;
   constexpr int kMaxDevices = 64;
@@ -831,7 +892,7 @@ static hipError_t set_lds_limit() {
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < kMaxDevices && done[dev].load(std::memory_order_relaxed)) return hipSuccess;
-  const void *kern = reinterpret_cast<const void *>(&chunk_local_kernel<T, DK, DV, KDA, PRE>);
+  const void *kern = reinterpret_cast<const void *>(&chunk_local_kernel<T, DK, DV, KDA, PRE, OVL>);
   if ((e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L::bytes)) != hipSuccess)
     return e;
   if (dev < kMaxDevices) done[dev].store(true, std::memory_order_relaxed);
@@ -868,6 +929,59 @@ hipError_t launch_chunk_local(const PrefillArgs &a, bool bf16, bool kda, hipStre
   if (a.max_chunks == 0) return hipSuccess;
   if (bf16) return kda ? dispatch_pre<bf16_t, true>(a, s) : dispatch_pre<bf16_t, false>(a, s);
   return kda ? dispatch_pre<float, true>(a, s) : dispatch_pre<float, false>(a, s);
+}
+
+// ------------------------------------------------------------ overlapped launch
+// One grid runs the chunk-local items and the whole-chain walks at once: the
+// walk of chunk c starts as soon as chunk c's factors exist instead of after
+// the last chunk-local block.  Walk workgroups come first in the grid, so
+// they are resident (each waits on its first chunk) before the chunk-local
+// workgroups fill the remaining slots; the chunk-local workgroups never wait,
+// so the launch always drains.  Both roles pick their work from queues of the
+// XCD they run on (xcc_id): the blocks of a head and its walks then share one
+// L2, through which the factors and the ready flags pass.  Every XCD gets
+// kOvlSlack workgroups of each role more than its share, so that a dispatch
+// that deals the grid a little unevenly over the XCDs still covers every
+// queue.
+constexpr int kOvlSlack = 2;
+
+__global__ __launch_bounds__(256) void overlap_setup_kernel(PrefillArgs a) {
+  const long n = kOvlFlags + (long)a.max_chunks * a.Hv;
+  for (long i = (long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long)gridDim.x * 256) a.ovl[i] = 0;
+  if (a.single && blockIdx.x == 0 && threadIdx.x == 0) a.status[0] = single_ok(a) ? 0 : kDevBadSeqlens;
+}
+
+hipError_t launch_overlap_setup(const PrefillArgs &a, hipStream_t stream) {
+  const long n = kOvlFlags + (long)a.max_chunks * a.Hv;
+  const long blocks = std::min<long>(256, (n + 255) / 256);
+  hipLaunchKernelGGL(overlap_setup_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+bool overlap_supported(bool bf16, int Dk, int Dv) { return bf16 && Dk == 128 && Dv == 128; }
+
+template <bool KDA, bool PRE, int OVL>
+static hipError_t launch_ovl_t(PrefillArgs a, hipStream_t stream) {
+  constexpr int DK = 128, DV = 128;
+  using L = LocalLayout<bf16_t, DK, DV, KDA>;
+  hipError_t e = set_lds_limit<bf16_t, DK, DV, KDA, PRE, OVL>();
+  if (e != hipSuccess) return e;
+  const long hx = ovl_heads(a.Hv, 0);  // the most heads any XCD serves
+  const long walks = kXcdCount * ((long)a.N * hx * (DV / 16) + kOvlSlack);
+  const long items = kXcdCount * ((long)a.max_chunks * hx + kOvlSlack);
+  a.ovl_walk_wgs = (int)walks;
+  hipLaunchKernelGGL((chunk_local_kernel<bf16_t, DK, DV, KDA, PRE, OVL>), dim3((unsigned)(walks + items)),
+                     dim3(kLocalThreads), L::bytes, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_overlapped(const PrefillArgs &a, bool kda, hipStream_t s) {
+  if (a.single) {
+    if (kda) return a.pre ? launch_ovl_t<true, true, 1>(a, s) : launch_ovl_t<true, false, 1>(a, s);
+    return a.pre ? launch_ovl_t<false, true, 1>(a, s) : launch_ovl_t<false, false, 1>(a, s);
+  }
+  if (kda) return a.pre ? launch_ovl_t<true, true, 2>(a, s) : launch_ovl_t<true, false, 2>(a, s);
+  return a.pre ? launch_ovl_t<false, true, 2>(a, s) : launch_ovl_t<false, false, 2>(a, s);
 }
 
 }  // namespace hagdn

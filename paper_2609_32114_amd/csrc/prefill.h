@@ -83,7 +83,35 @@ struct PrefillArgs {
   // the tables below from T and cu_seqlens (seq_info_at and friends)
   int single;
   int cus;             // compute units of the device the call runs on
+  // Overlapped launch (the chunk-local work and the whole-chain walks in one
+  // grid, launch_overlapped): workgroups [0, ovl_walk_wgs) walk, the rest run
+  // chunk-local items.  ovl holds, per XCD x, a chunk-local item queue at
+  // kOvlLocalQ + kOvlStride x and a walk tile queue at kOvlWalkQ + kOvlStride x
+  // (each in its own 128-byte line), then a ready flag per (chunk, value head)
+  // block at kOvlFlags + blk.  All zero before the launch (overlap_setup).
+  int *ovl;
+  int ovl_walk_wgs;
 };
+
+// XCDs of an MI355X.  Each has its own L2; the L2s are not coherent with each
+// other within a kernel.
+constexpr int kXcdCount = 8;
+constexpr int kOvlStride = 32;                           // ints: one 128-byte line per queue
+constexpr int kOvlLocalQ = 0;
+constexpr int kOvlWalkQ = kXcdCount * kOvlStride;
+constexpr int kOvlFlags = 2 * kXcdCount * kOvlStride;     // 2 KiB in
+// Device status codes (hagdn_device_code).
+constexpr int kDevBadSeqlens = 1;
+constexpr int kDevWaitTimeout = 2;
+
+// Id of the XCD the calling wave runs on.
+__device__ __forceinline__ int xcc_id() {
+  int x;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+  return x & (kXcdCount - 1);
+}
+// Value heads served by XCD x in an overlapped launch: h = x, x + 8, ...
+__host__ __device__ __forceinline__ int ovl_heads(int Hv, int x) { return Hv > x ? (Hv - x + kXcdCount - 1) / kXcdCount : 0; }
 
 // The tables of the chunk index kernel, or for a single sequence (SINGLE:
 // the kernels' separate instances for N = 1) the same entries derived in
@@ -156,6 +184,13 @@ hipError_t launch_chunk_index(const PrefillArgs &a, hipStream_t stream);
 hipError_t launch_chunk_local(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
 // ops #5 + #6 over whole chains (every sequence one segment)
 hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
+// Whether launch_overlapped has an instance for these operands.
+bool overlap_supported(bool bf16, int Dk, int Dv);
+// Zeroes the overlap queues and flags (and for a single sequence writes the
+// device status word, which no chunk index kernel then writes).
+hipError_t launch_overlap_setup(const PrefillArgs &a, hipStream_t stream);
+// Chunk-local items and whole-chain walks in one launch (k1_chunk_local.hip).
+hipError_t launch_overlapped(const PrefillArgs &a, bool kda, hipStream_t stream);
 // the bf16 whole-chain walk for batches with more walks than the device's
 // compute units (a.cus; k2_walk.hip)
 hipError_t launch_state_walk(const PrefillArgs &a, bool kda, int cus, hipStream_t stream);

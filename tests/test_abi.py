@@ -120,6 +120,29 @@ def test_segment_rule_depends_on_the_cu_count():
         assert P.segment_chunks(1, 32768, 16, 128) == P.segment_chunks_for(1, 32768, 16, 128, 256)
 
 
+@needs_lib
+def test_overlap_rule():
+    """Which calls take the overlapped launch: bf16 with d_k = d_v = 128, chains
+    walked whole, walks on at most half the CUs of a device of 8 XCDs."""
+    bf, f32 = P.HAGDN_BF16, P.HAGDN_F32
+    assert P.overlap_for(1, 4096, 16, 128, 128, bf, "gdn", 256)
+    assert P.overlap_for(1, 4096, 16, 128, 128, bf, "kda", 256)
+    assert P.overlap_for(5, 900, 2, 128, 128, bf, "gdn", 256)
+    assert not P.overlap_for(1, 4096, 16, 128, 128, f32, "gdn", 256)      # no fp32 instance
+    assert not P.overlap_for(1, 4096, 16, 64, 128, bf, "gdn", 256)        # no d_k = 64 instance
+    assert not P.overlap_for(1, 4096, 32, 128, 128, bf, "gdn", 256)       # 256 walks: every CU
+    assert not P.overlap_for(1, 32768, 16, 128, 128, bf, "gdn", 256)      # segment maps
+    assert not P.overlap_for(1, 4096, 16, 128, 128, bf, "gdn", 128)       # fewer than 8 x 32 CUs
+    assert not P.overlap_for(1, 0, 16, 128, 128, bf, "gdn", 256)          # nothing to launch
+    try:
+        P.set_overlap(False)
+        assert not P.overlap_for(1, 4096, 16, 128, 128, bf, "gdn", 256)
+    finally:
+        P.set_overlap(True)
+    with pytest.raises(P.HagdnError):
+        P.overlap_for(1, 4096, 16, 128, 128, bf, "gdn", 0)
+
+
 def test_segment_length_knob():
     import paper_2609_32114_amd as P
     P.load_library()
