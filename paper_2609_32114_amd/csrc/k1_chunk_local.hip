@@ -319,9 +319,10 @@ struct LocalIn {
 
 // PRE: the call carries preprocessing flags (a separate instance, so that the
 // plain path keeps its register budget).  OVL: the overlapped launch (1: a
-// single sequence, 2: a batch): workgroups below a.ovl_walk_wgs walk whole
-// chains (ovl_walk), the others take chunk-local items from their XCD's
-// queue and publish each block's ready flag once its factors are stored.
+// single sequence, 2: a batch): every workgroup takes a chunk-local item from
+// its XCD's queue and publishes the block's ready flag once its factors are
+// stored; workgroups below a.ovl_walk_wgs then walk a whole chain
+// (ovl_walk).
 template <typename T, int DK, int DV, bool KDA, bool PRE, int OVL = 0>
 __global__ __launch_bounds__(kLocalThreads, OVL || (KDA && sizeof(T) == 2) ? 2 : 1) void chunk_local_kernel(PrefillArgs a) {
   using L = LocalLayout<T, DK, DV, KDA>;
@@ -333,14 +334,16 @@ __global__ __launch_bounds__(kLocalThreads, OVL || (KDA && sizeof(T) == 2) ? 2 :
   constexpr int KPW = KT / 4;             // d_k tiles per wave in the reduce-side products
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int col = lane & 15, grp = lane >> 4;
-  if constexpr (OVL != 0) {
-    if ((int)blockIdx.x < a.ovl_walk_wgs) {
-      ovl_walk<T, DK, DV, KDA, OVL == 1>(a);
-      return;
-    }
-  }
+  // overlapped launch: walk workgroups also produce one chunk-local item
+  // first, while the first chunks are being computed everywhere
+  const bool walker = OVL != 0 && (int)blockIdx.x < a.ovl_walk_wgs;
   const LocalItem cur = OVL ? ovl_item(a) : local_item(a, blockIdx.x);
-  if (cur.len <= 0) return;  // past the last chunk: uniform for the workgroup
+  if (cur.len <= 0) {  // past the last chunk: uniform for the workgroup
+    if constexpr (OVL != 0) {
+      if (walker) ovl_walk<T, DK, DV, KDA, OVL == 1>(a);
+    }
+    return;
+  }
   In in;
   in.load_kvg(a, cur);
   in.load_q(a, cur);
@@ -878,6 +881,10 @@ __global__ __launch_bounds__(kLocalThreads, OVL || (KDA && sizeof(T) == 2) ? 2 :
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (tid == 0) __hip_atomic_fetch_or(a.ovl + kOvlFlags + blk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (walker) {
+      __syncthreads();  // the walk's exchange buffer reuses this item's LDS
+      ovl_walk<T, DK, DV, KDA, OVL == 1>(a);
+    }
   }
 }
 
