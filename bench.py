@@ -186,6 +186,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--segment-chunks", type=int, default=0,
                     help="segment length of the state chain in 64-token chunks (0: automatic)")
+    ap.add_argument("--no-overlap", action="store_true",
+                    help="run the chunk-local kernel and the state walks one after another even where "
+                         "the overlapped launch applies")
     ap.add_argument("--pre", action="store_true",
                     help="prefill from raw projections with every in-kernel preprocessing flag")
     ap.add_argument("--decode", action="store_true", help="time the decode step instead of prefill")
@@ -232,6 +235,7 @@ def main():
 
     P.load_library()
     P.set_segment_chunks(args.segment_chunks)
+    P.set_overlap(not args.no_overlap)
     wl = WORKLOADS[args.workload]
     pre = P.PRE_ALL if args.pre else 0
     inp = make_workload(args.workload, raw=bool(pre))
@@ -325,7 +329,9 @@ def main():
         "config": {"workload": wname, "kind": inp.kind, "sequences": N, "seq_len": T,
                    "q_k_heads": Hqk, "v_heads": Hv, "head_dim_k": Dk, "head_dim_v": Dv,
                    "chunk": 64, "segment_chunks": L, "input_copies": len(copies),
-                   "preprocess": pre},
+                   "preprocess": pre,
+                   "overlapped": P.overlap_for(N, T, Hv, Dk, Dv, P.HAGDN_BF16 if esz == 2 else P.HAGDN_F32,
+                                               inp.kind, torch.cuda.get_device_properties(0).multi_processor_count)},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "algorithmic_bytes": path_bytes, "kernel_ms": dom_ms},
