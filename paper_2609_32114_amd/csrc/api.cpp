@@ -132,6 +132,9 @@ int seg_chunks(int N, int T, int Hv, int Dv, size_t esz, bool kda, int cus) {
   return (int)std::min(L, cap);
 }
 
+// Chunks of a T-token sequence (64-bit: T + 63 overflows int near INT_MAX).
+long chunks_of(int T) { return ((long)T + hagdn::kChunk - 1) / hagdn::kChunk; }
+
 bool mul_ok(size_t a, size_t b, size_t *out) { return !__builtin_mul_overflow(a, b, out); }
 bool add_ok(size_t a, size_t b, size_t *out) { return !__builtin_add_overflow(a, b, out); }
 
@@ -178,7 +181,7 @@ bool make_layout(int N, int T, int Hv, int Dk, int Dv, size_t esz, bool kda, int
   L->seq_seg = region(1, sizeof(int2), (size_t)N);
   L->seg_info = region(1, sizeof(int4), ms);
   // segment maps exist only when a sequence can span two segments
-  const bool maps = (size_t)(T + hagdn::kChunk - 1) / hagdn::kChunk > (size_t)L->seg_chunks;
+  const bool maps = chunks_of(T) > L->seg_chunks;
   L->Aseg = region((size_t)Dk * Dk, esz, maps ? sblocks : 0);
   L->Bseg = region((size_t)Dk * Dv, sizeof(float), maps ? sblocks : 0);
   L->s0c = region((size_t)Dk * Dv, sizeof(float), maps ? (size_t)N * (size_t)Hv : 0);
@@ -295,7 +298,7 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   a.cus = cus;
   a.ovl = reinterpret_cast<int *>(w + L.ovl);
   a.ovl_walk_wgs = 0;
-  const bool maps = (T + hagdn::kChunk - 1) / hagdn::kChunk > L.seg_chunks;
+  const bool maps = chunks_of(T) > L.seg_chunks;
   const bool overlap = T > 0 && overlap_applies(bf16, Dk, Dv, maps, N, Hv, cus);
 
   hipStream_t st = static_cast<hipStream_t>(stream_);
@@ -571,7 +574,7 @@ int hagdn_overlap_for(int N, int T_total, int Hv, int Dk, int Dv, int dtype, int
   if (cus < 1) return fail(HAGDN_EINVAL, "cus must be >= 1 (got %d)", cus), -1;
   const size_t esz = dtype == HAGDN_BF16 ? 2 : 4;
   const int L = seg_chunks(N, T_total, Hv, Dv, esz, kda != 0, cus);
-  const bool maps = (T_total + hagdn::kChunk - 1) / hagdn::kChunk > L;
+  const bool maps = chunks_of(T_total) > L;
   return T_total > 0 && overlap_applies(dtype == HAGDN_BF16, Dk, Dv, maps, N, Hv, cus) ? 1 : 0;
 }
 

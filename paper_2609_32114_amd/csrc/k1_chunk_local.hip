@@ -965,8 +965,6 @@ hipError_t launch_overlap_setup(const PrefillArgs &a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-bool overlap_supported(bool bf16, int Dk, int Dv) { return bf16 && Dk == 128 && Dv == 128; }
-
 template <bool KDA, bool PRE, int OVL>
 static hipError_t launch_ovl_t(PrefillArgs a, hipStream_t stream) {
   constexpr int DK = 128, DV = 128;

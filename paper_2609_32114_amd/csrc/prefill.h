@@ -184,8 +184,8 @@ hipError_t launch_chunk_index(const PrefillArgs &a, hipStream_t stream);
 hipError_t launch_chunk_local(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
 // ops #5 + #6 over whole chains (every sequence one segment)
 hipError_t launch_state_prop(const PrefillArgs &a, bool bf16, bool kda, hipStream_t stream);
-// Whether launch_overlapped has an instance for these operands.
-bool overlap_supported(bool bf16, int Dk, int Dv);
+// launch_overlapped has instances for bf16 with Dk = Dv = 128.
+inline bool overlap_supported(bool bf16, int Dk, int Dv) { return bf16 && Dk == 128 && Dv == 128; }
 // Zeroes the overlap queues and flags (and for a single sequence writes the
 // device status word, which no chunk index kernel then writes).
 hipError_t launch_overlap_setup(const PrefillArgs &a, hipStream_t stream);
