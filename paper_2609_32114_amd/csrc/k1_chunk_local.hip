@@ -187,13 +187,20 @@ __device__ __forceinline__ void ovl_walk(const PrefillArgs &a) {
   constexpr int NT = DV / 16;
   __shared__ int ticket;
   const int x = xcc_id();
-  if (threadIdx.x == 0) ticket = atomicAdd(a.ovl + kOvlWalkQ + kOvlStride * x, 1);
-  __syncthreads();
-  const int t = ticket;
   const int hx = ovl_heads(a.Hv, x);
-  if (hx == 0 || t >= a.N * hx * NT) return;  // uniform for the workgroup
-  const int j = t / NT, n = j / hx, h = x + kXcdCount * (j % hx);
-  walk_tile<T, DK, DV, KDA, SINGLE, true>(a, n * a.Hv + h, t % NT);
+  // A walker takes tiles until its XCD's queue is empty: the grid gives every
+  // XCD its share and two more, and should a dispatch deal the grid unevenly,
+  // the walkers that did land on an XCD still walk all of its tiles.
+  for (;;) {
+    if (threadIdx.x == 0) ticket = atomicAdd(a.ovl + kOvlWalkQ + kOvlStride * x, 1);
+    __syncthreads();
+    const int t = ticket;
+    __syncthreads();  // every wave has read the ticket before the next one is taken
+    if (hx == 0 || t >= a.N * hx * NT) return;  // uniform for the workgroup
+    const int j = t / NT, n = j / hx, h = x + kXcdCount * (j % hx);
+    walk_tile<T, DK, DV, KDA, SINGLE, true>(a, n * a.Hv + h, t % NT);
+    __syncthreads();  // the walk's exchange buffer is free again
+  }
 }
 
 // Global inputs of one item (padded tokens: zeros).
