@@ -73,12 +73,14 @@ template <typename T, bool KDA> constexpr int pipe_depth() {
   return sizeof(T) == 2 ? (KDA ? 2 : 3) : 2;
 }
 
-// Ready-flag polling of an overlapped walk.  A flag is read with an atomic
-// (fetch-or of 0), which executes in this XCD's L2 -- where the chunk-local
-// blocks of this head stored their factors and then set the flag with an
-// atomic -- and never in the CU's L1, which would keep serving the value of
-// the first read.  Between polls a wave sleeps kOvlSleep x 64 cycles; after
-// kOvlMaxPolls polls it stops waiting and reports HAGDN_DEV_WAIT_TIMEOUT.
+// Ready-flag polling of an overlapped walk.  A flag is read with an
+// agent-scope atomic load (global_load sc1), which skips the CU's L1 and is
+// served by this XCD's L2 -- where the chunk-local blocks of this head stored
+// their factors and then set the flag with an atomic.  A workgroup-scope load
+// (sc0) was served from the L1 and kept returning the first value it read; an
+// atomic read-modify-write works too but cost the walk ~10 % per step.
+// Between polls a wave sleeps kOvlSleep x 64 cycles; after kOvlMaxPolls polls
+// it stops waiting and reports HAGDN_DEV_WAIT_TIMEOUT.
 constexpr int kOvlSleep = 8;
 constexpr int kOvlMaxPolls = 1 << 21;
 
@@ -198,7 +200,7 @@ __device__ __forceinline__ void walk_tile(const PrefillArgs &a, int pair, int ti
     bool timed_out = false;
     int *const flags = a.ovl + kOvlFlags;
     auto ovl_flag = [&](int c) {
-      return __hip_atomic_fetch_or(flags + blk(c), 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return __hip_atomic_load(flags + blk(c), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     };
     auto ovl_wait = [&](int flag, int c) {
       int v = __builtin_amdgcn_readfirstlane(flag);
