@@ -333,7 +333,6 @@ struct LocalIn {
 template <typename T, int DK, int DV, bool KDA, bool PRE, int OVL = 0>
 __global__ __launch_bounds__(kLocalThreads, OVL || (KDA && sizeof(T) == 2) ? 2 : 1) void chunk_local_kernel(PrefillArgs a) {
   using L = LocalLayout<T, DK, DV, KDA>;
-  using E = Elt<T>;
   using V16 = Vec16<T>;
   using In = LocalIn<T, DK, DV, KDA, PRE>;
   constexpr int V = 16 / (int)sizeof(T);  // elements per 16-byte vector
