@@ -106,3 +106,24 @@ def test_overlap_workload1_every_head():
         P.set_overlap(True)
     np.testing.assert_array_equal(o_ovl, o_ser)
     np.testing.assert_array_equal(s_ovl, s_ser)
+
+
+@pytest.mark.parametrize("kind", ["gdn", "kda"])
+def test_overlap_in_place_state(kind):
+    """s_final aliasing s0 on the overlapped launch: every walk reads its
+    columns of s0 before it writes them, and no producer touches the state."""
+    import torch
+    import paper_2609_32114_amd as P
+    inp = make_case(kind, (777,), 4, 16, 128, 128, "bf16", with_s0=True, variant="s0", seed=43)
+    assert P.overlap_for(1, 777, 16, 128, 128, P.HAGDN_BF16, kind)
+    d = to_device(inp)
+    fn = P.gdn_prefill if kind == "gdn" else P.kda_prefill
+    o_ref, s_ref = fn(d["q"], d["k"], d["v"], d["g"], d["beta"], initial_state=d["s0"], cu_seqlens=d["cu"],
+                      scale=inp.scale)
+    state = d["s0"].clone()
+    o, sf = fn(d["q"], d["k"], d["v"], d["g"], d["beta"], initial_state=state, cu_seqlens=d["cu"],
+               scale=inp.scale, final_out=state)
+    torch.cuda.synchronize()
+    assert sf.data_ptr() == state.data_ptr()
+    np.testing.assert_array_equal(state.cpu().numpy(), s_ref.cpu().numpy())
+    np.testing.assert_array_equal(o.float().cpu().numpy(), o_ref.float().cpu().numpy())
