@@ -85,7 +85,7 @@ typedef enum { HAGDN_F32 = 0, HAGDN_BF16 = 1 } hagdn_dtype;
 /* Device-side status word written by every prefill call (by its first
  * kernel, or for a single sequence by its state kernel or, in an overlapped
  * call, by the setup kernel).  HAGDN_DEV_WAIT_TIMEOUT: in an overlapped call
- * (hagdn_set_overlap) a walk stopped waiting, after about 0.4 s, for a chunk
+ * (hagdn_set_overlap) a walk stopped waiting, after about a second, for a chunk
  * that its XCD's chunk-local work never published; the outputs are invalid.
  * Not expected: it would take a dispatch that leaves some XCD without the
  * workgroups of its queue (see hagdn_set_overlap). */
@@ -255,27 +255,29 @@ int hagdn_segment_chunks_for(int N, int T_total, int Hv, int Dv, int dtype, int 
 
 /* Overlapped launch.  The state walk of chunk c needs only chunks 0..c's
  * chunk-local factors, so a call whose chains are walked whole (no segment
- * maps: see hagdn_segment_chunks) runs the chunk-local work (operators #1-#4
- * and the state-independent factors of #5-#6) and the walks (#5 fused with #6)
- * in ONE launch: walk workgroups wait, chunk by chunk, for ready flags that the
- * chunk-local workgroups set once a block's factors are stored, instead of
- * for the whole chunk-local kernel (Sec. 4's cross-operator fusion, with the
- * Map of later chunks running beside the Reduce of earlier ones).  Each
- * workgroup reads the id of the XCD it runs on and takes its work from that
- * XCD's queues: value heads h = x (mod 8) are produced and walked on XCD x,
- * so the factors and flags pass through one L2 (the L2s of different XCDs are
- * not coherent within a kernel).  It applies to bf16 calls with Dk = Dv = 128,
- * on devices of at least 256 CUs (8 XCDs), whose walks (N x Hv x Dv/16
- * workgroups) fit in half the CUs; other calls run the kernels one after
- * another.  Results are bit-identical either way.  A tiny setup kernel clears
- * the queues and flags first (in the workspace).  hagdn_set_overlap(0) turns
- * it off for every later call in the process, (1) back on (the default).
- * Returns HAGDN_OK or HAGDN_EINVAL. */
-int hagdn_set_overlap(int on);
+ * maps: see hagdn_segment_chunks) can run the chunk-local work (operators
+ * #1-#4 and the state-independent factors of #5-#6) and the walks (#5 fused
+ * with #6) in ONE launch: walk workgroups wait, chunk by chunk, for ready flags
+ * that the chunk-local workgroups set once a block's factors are stored,
+ * instead of for the whole chunk-local kernel (Sec. 4's cross-operator fusion,
+ * with the Map of later chunks running beside the Reduce of earlier ones).
+ * Each workgroup reads the id of the XCD it runs on and takes its work from
+ * that XCD's queues: value heads h = x (mod 8) are produced and walked on XCD
+ * x, so the factors and flags pass through one L2 (the L2s of different XCDs
+ * are not coherent within a kernel).  It can run for GDN calls in bf16 with
+ * Dk = Dv = 128 on devices of at least 256 CUs (8 XCDs) whose walks (N x Hv x
+ * Dv/16 workgroups) fit in half the CUs.  It pays only when the chunk-local
+ * work needs more than one round of the standalone kernel (more than 3 x CUs
+ * (chunk, value head) blocks): mode 1, the default, uses it exactly then;
+ * mode 2 wherever it can run (for tests and measurements); mode 0 never.
+ * Results are bit-identical either way.  A tiny setup kernel clears the
+ * queues and flags first (in the workspace).  Applies to every later call in
+ * the process.  Returns HAGDN_OK or HAGDN_EINVAL. */
+int hagdn_set_overlap(int mode);
 
 /* 1 if a call with these sizes (kda: 0 gdn, 1 kda) would take the overlapped
- * launch on a device of `cus` compute units with the switch as it is now, 0
- * if not, -1 on invalid arguments.  Host logic only. */
+ * launch on a device of `cus` compute units in the mode set now, 0 if not, -1
+ * on invalid arguments.  Host logic only. */
 int hagdn_overlap_for(int N, int T_total, int Hv, int Dk, int Dv, int dtype, int kda, int cus);
 
 /* Allocation-free prefill, for callers that cannot allocate device memory

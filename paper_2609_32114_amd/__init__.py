@@ -305,11 +305,11 @@ def set_segment_chunks(chunks: int):
         raise HagdnError(rc, _err(lib))
 
 
-def set_overlap(on: bool):
-    """Whether later calls that qualify run the chunk-local work and the state
-    walks in one overlapped launch (True, the default) or one after another."""
+def set_overlap(on: bool = True, force: bool = False):
+    """The overlapped launch for later calls: where it pays (on, the default),
+    wherever it can run (force; for tests and measurements), or never (off)."""
     lib = load_library()
-    rc = lib.hagdn_set_overlap(1 if on else 0)
+    rc = lib.hagdn_set_overlap(0 if not on else (2 if force else 1))
     if rc != 0:
         raise HagdnError(rc, _err(lib))
 

@@ -52,8 +52,8 @@ constexpr int kDecodeKernel = 4;
 
 // Chunks per segment of the state chain; 0 = chosen per call (seg_chunks).
 std::atomic<int> g_seg_override{0};
-// 1: calls that can run the chunk-local work and the state walks in one
-// overlapped launch do so (hagdn_set_overlap).
+// The overlapped launch (hagdn_set_overlap): 0 never, 1 where it pays (the
+// default), 2 wherever it can run (overlap_applies).
 std::atomic<int> g_overlap{1};
 constexpr int kMaxSegChunks = 1 << 20;
 // Compute units assumed by the size and segment-length queries when no HIP
@@ -206,15 +206,27 @@ int check_shapes(int N, int T, int Hqk, int Hv, int Dk, int Dv, int dtype) {
 }
 
 // Whether a call runs the chunk-local kernel and the whole-chain walks in one
-// overlapped launch (k1_chunk_local.hip, launch_overlapped): chains walked
-// whole by the four-wave walk, an instance for the operands, a device of at
-// least 8 XCDs x 32 CUs (XCC ids 0-7) and walks on at most half the CUs, so
-// that the chunk-local work keeps most of the device.
-bool overlap_applies(bool bf16, int Dk, int Dv, bool maps, int N, int Hv, int cus) {
-  if (!g_overlap.load(std::memory_order_relaxed) || maps || !hagdn::overlap_supported(bf16, Dk, Dv)) return false;
+// overlapped launch (k1_chunk_local.hip, launch_overlapped).  It needs chains
+// walked whole by the four-wave walk (no segment maps), an instance for the
+// operands (overlap_supported), a device of at least 8 XCDs x 32 CUs (XCC ids
+// 0-7) and walks on at most half the CUs, so that the chunk-local work keeps
+// most of the device.  In the automatic mode it also needs more chunk-local
+// blocks than one round of the standalone kernel (3 per CU): the overlapped
+// call costs about 20 us until the first chunk is ready plus the walk at
+// ~0.88 us per chunk, against the standalone chunk-local kernel plus the walk
+// at ~0.74 us per chunk, so it pays once the chunk-local kernel needs a second
+// round.  Single sequences, d = 128, 256 CUs (us per call, overlapped against
+// serialized, interleaved in one process): 4096 tokens x 16 heads (1040
+// blocks) 88.9 / 92.3; 6144 x 16 (1552) 120.5 / 128.2; 2048 x 16 (528) 55.0 /
+// 52.1; 4096 x 8 (520) 76.4 / 71.9.
+bool overlap_applies(bool bf16, bool kda, int Dk, int Dv, bool maps, int N, int T, int Hv, int cus) {
+  const int mode = g_overlap.load(std::memory_order_relaxed);
+  if (mode == 0 || maps || !hagdn::overlap_supported(bf16, kda, Dk, Dv)) return false;
   if (cus < hagdn::kXcdCount * 32) return false;
   const long walks = (long)N * Hv * (Dv / 16);
-  return walks <= cus / 2;
+  if (walks > cus / 2) return false;
+  const long blocks = ((long)T / hagdn::kChunk + N) * Hv;  // chunk-local blocks (an upper bound)
+  return mode == 2 || blocks > 3L * cus;
 }
 
 size_t workspace_size(bool kda, int N, int T, int Hqk, int Hv, int Dk, int Dv, int dtype) {
@@ -299,7 +311,7 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
   a.ovl = reinterpret_cast<int *>(w + L.ovl);
   a.ovl_walk_wgs = 0;
   const bool maps = chunks_of(T) > L.seg_chunks;
-  const bool overlap = T > 0 && overlap_applies(bf16, Dk, Dv, maps, N, Hv, cus);
+  const bool overlap = T > 0 && overlap_applies(bf16, kda, Dk, Dv, maps, N, T, Hv, cus);
 
   hipStream_t st = static_cast<hipStream_t>(stream_);
   hipEvent_t *ev = nullptr;
@@ -328,7 +340,7 @@ int prefill(bool kda, const void *q, const void *k, const void *v, const float *
     // then the chunk-local items and the walks in one launch
     if ((e = hagdn::launch_overlap_setup(a, st)) != hipSuccess) goto hip_fail;
     if ((e = mark(6)) != hipSuccess) goto hip_fail;
-    if ((e = hagdn::launch_overlapped(a, kda, st)) != hipSuccess) goto hip_fail;
+    if ((e = hagdn::launch_overlapped(a, st)) != hipSuccess) goto hip_fail;
     if ((e = mark(7)) != hipSuccess) goto hip_fail;
     return HAGDN_OK;
   }
@@ -563,9 +575,9 @@ const char *hagdn_kernel_name(int i) { return (i >= 0 && i < kNumKernels) ? kKer
 
 int hagdn_version(void) { return 100; }
 
-int hagdn_set_overlap(int on) {
-  if (on != 0 && on != 1) return fail(HAGDN_EINVAL, "overlap switch must be 0 or 1 (got %d)", on);
-  g_overlap.store(on, std::memory_order_relaxed);
+int hagdn_set_overlap(int mode) {
+  if (mode < 0 || mode > 2) return fail(HAGDN_EINVAL, "overlap mode must be 0, 1 or 2 (got %d)", mode);
+  g_overlap.store(mode, std::memory_order_relaxed);
   return HAGDN_OK;
 }
 
@@ -575,7 +587,7 @@ int hagdn_overlap_for(int N, int T_total, int Hv, int Dk, int Dv, int dtype, int
   const size_t esz = dtype == HAGDN_BF16 ? 2 : 4;
   const int L = seg_chunks(N, T_total, Hv, Dv, esz, kda != 0, cus);
   const bool maps = chunks_of(T_total) > L;
-  return T_total > 0 && overlap_applies(dtype == HAGDN_BF16, Dk, Dv, maps, N, Hv, cus) ? 1 : 0;
+  return T_total > 0 && overlap_applies(dtype == HAGDN_BF16, kda != 0, Dk, Dv, maps, N, T_total, Hv, cus) ? 1 : 0;
 }
 
 int hagdn_set_segment_chunks(int chunks) {

@@ -986,12 +986,8 @@ static hipError_t launch_ovl_t(PrefillArgs a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-hipError_t launch_overlapped(const PrefillArgs &a, bool kda, hipStream_t s) {
-  if (a.single) {
-    if (kda) return a.pre ? launch_ovl_t<true, true, 1>(a, s) : launch_ovl_t<true, false, 1>(a, s);
-    return a.pre ? launch_ovl_t<false, true, 1>(a, s) : launch_ovl_t<false, false, 1>(a, s);
-  }
-  if (kda) return a.pre ? launch_ovl_t<true, true, 2>(a, s) : launch_ovl_t<true, false, 2>(a, s);
+hipError_t launch_overlapped(const PrefillArgs &a, hipStream_t s) {
+  if (a.single) return a.pre ? launch_ovl_t<false, true, 1>(a, s) : launch_ovl_t<false, false, 1>(a, s);
   return a.pre ? launch_ovl_t<false, true, 2>(a, s) : launch_ovl_t<false, false, 2>(a, s);
 }
 

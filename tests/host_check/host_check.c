@@ -74,7 +74,12 @@ static void rules(void) {
   EXPECT(hagdn_segment_chunks_for(1, 100, 16, 128, HAGDN_BF16, 0, 0) == -1);
   EXPECT(hagdn_overlap_for(1, 100, 16, 128, 128, HAGDN_BF16, 0, 0) == -1);
   EXPECT(hagdn_overlap_for(1, 4096, 16, 128, 128, HAGDN_BF16, 0, 256) == 1);
-  EXPECT(hagdn_set_overlap(2) == HAGDN_EINVAL);
+  EXPECT(hagdn_set_overlap(3) == HAGDN_EINVAL);
+  EXPECT(hagdn_set_overlap(-1) == HAGDN_EINVAL);
+  EXPECT(hagdn_overlap_for(1, 2048, 16, 128, 128, HAGDN_BF16, 0, 256) == 0);
+  EXPECT(hagdn_set_overlap(2) == HAGDN_OK);
+  EXPECT(hagdn_overlap_for(1, 2048, 16, 128, 128, HAGDN_BF16, 0, 256) == 1);
+  EXPECT(hagdn_overlap_for(1, 2048, 16, 128, 128, HAGDN_BF16, 1, 256) == 0);
   EXPECT(hagdn_set_overlap(0) == HAGDN_OK);
   EXPECT(hagdn_overlap_for(1, 4096, 16, 128, 128, HAGDN_BF16, 0, 256) == 0);
   EXPECT(hagdn_set_overlap(1) == HAGDN_OK);

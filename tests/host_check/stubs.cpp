@@ -9,7 +9,7 @@ hipError_t launch_chunk_index(const PrefillArgs &, hipStream_t) { return hipErro
 hipError_t launch_chunk_local(const PrefillArgs &, bool, bool, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_state_prop(const PrefillArgs &, bool, bool, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_overlap_setup(const PrefillArgs &, hipStream_t) { return hipErrorNoDevice; }
-hipError_t launch_overlapped(const PrefillArgs &, bool, hipStream_t) { return hipErrorNoDevice; }
+hipError_t launch_overlapped(const PrefillArgs &, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_state_walk(const PrefillArgs &, bool, int, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_seg_maps(const PrefillArgs &, bool, hipStream_t) { return hipErrorNoDevice; }
 hipError_t launch_seg_transfer(const PrefillArgs &, bool, bool, hipStream_t) { return hipErrorNoDevice; }

@@ -122,12 +122,15 @@ def test_segment_rule_depends_on_the_cu_count():
 
 @needs_lib
 def test_overlap_rule():
-    """Which calls take the overlapped launch: bf16 with d_k = d_v = 128, chains
-    walked whole, walks on at most half the CUs of a device of 8 XCDs."""
+    """Which calls take the overlapped launch: GDN in bf16 with d_k = d_v = 128,
+    chains walked whole, walks on at most half the CUs of a device of 8 XCDs,
+    and (by default) more chunk-local blocks than one round of 3 per CU."""
     bf, f32 = P.HAGDN_BF16, P.HAGDN_F32
-    assert P.overlap_for(1, 4096, 16, 128, 128, bf, "gdn", 256)
-    assert P.overlap_for(1, 4096, 16, 128, 128, bf, "kda", 256)
-    assert P.overlap_for(5, 900, 2, 128, 128, bf, "gdn", 256)
+    assert P.overlap_for(1, 4096, 16, 128, 128, bf, "gdn", 256)           # 1040 blocks > 768
+    assert P.overlap_for(1, 6144, 16, 128, 128, bf, "gdn", 256)
+    assert not P.overlap_for(1, 2048, 16, 128, 128, bf, "gdn", 256)       # 528 blocks: one round
+    assert not P.overlap_for(1, 4096, 8, 128, 128, bf, "gdn", 256)        # 520 blocks
+    assert not P.overlap_for(1, 4096, 16, 128, 128, bf, "kda", 256)       # no KDA instance
     assert not P.overlap_for(1, 4096, 16, 128, 128, f32, "gdn", 256)      # no fp32 instance
     assert not P.overlap_for(1, 4096, 16, 64, 128, bf, "gdn", 256)        # no d_k = 64 instance
     assert not P.overlap_for(1, 4096, 32, 128, 128, bf, "gdn", 256)       # 256 walks: every CU
@@ -135,6 +138,10 @@ def test_overlap_rule():
     assert not P.overlap_for(1, 4096, 16, 128, 128, bf, "gdn", 128)       # fewer than 8 x 32 CUs
     assert not P.overlap_for(1, 0, 16, 128, 128, bf, "gdn", 256)          # nothing to launch
     try:
+        P.set_overlap(True, force=True)
+        assert P.overlap_for(1, 2048, 16, 128, 128, bf, "gdn", 256)
+        assert P.overlap_for(5, 900, 2, 128, 128, bf, "gdn", 256)
+        assert not P.overlap_for(1, 4096, 16, 128, 128, bf, "kda", 256)
         P.set_overlap(False)
         assert not P.overlap_for(1, 4096, 16, 128, 128, bf, "gdn", 256)
     finally:

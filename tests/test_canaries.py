@@ -36,9 +36,9 @@ def _guards_intact(raw, nbytes):
 
 
 CASES = [
-    # kind, lengths, Hqk, Hv, D, dtype, segment chunks (0: automatic), overlap
+    # kind, lengths, Hqk, Hv, D, dtype, segment chunks (0: automatic), overlap forced where it can run
     ("gdn", (1000,), 4, 16, 128, "bf16", 0, True),          # overlapped launch
-    ("gdn", (1000,), 4, 16, 128, "bf16", 0, False),         # serialized four-wave walk
+    ("gdn", (1000,), 4, 16, 128, "bf16", 0, False),         # serialized four-wave walk (too short to overlap)
     ("gdn", (300, 0, 1, 777), 12, 12, 128, "bf16", 0, True),  # staged walk: 384 walks
     ("kda", (1000,), 2, 8, 128, "bf16", 3, True),           # bf16 segment maps + segment walks
     ("gdn", (700, 65), 2, 6, 64, "f32", 4, True),           # fp32 maps, d = 64
@@ -59,7 +59,7 @@ def test_prefill_writes_stay_inside_buffers(case):
     esz = 2 if dtype == "bf16" else 4
     try:
         P.set_segment_chunks(L)
-        P.set_overlap(ovl)
+        P.set_overlap(True, force=ovl)
         code = P.HAGDN_BF16 if dtype == "bf16" else P.HAGDN_F32
         wsb = P.workspace_size(kind, N, T, Hqk, Hv, D, D, code)
         ws_raw, ws = _guarded(wsb, torch.uint8, None)
